@@ -1,0 +1,274 @@
+#!/usr/bin/env python3
+"""Throughput of dense C = A * B on one MI355X: FP16->FP32, INT8->INT32 and
+INT4->INT32 at square N in {512, 1024, 2048, 4096, 8192}.
+
+One step is one pass over the whole precision x size sweep: 15 GEMMs, each on
+its own seeded synthetic operands (seeds 10..24, FP16 U[-1,1], INT8 uniform
+over [-128, 127], INT4 uniform over [-8, 7] packed two per byte), already
+resident in HBM. Every GEMM goes through the library's C ABI on one stream.
+Ops per GEMM are 2*N^3 (the paper's convention: its Table II TOPS column is
+2*N^3 / duration).
+
+Printed: one JSON line on stdout (progress goes to stderr) with
+  value      whole-step throughput, total ops / wall time per step (TOP/s);
+  points     per-GEMM mean duration (HIP events on the launch stream, over the
+             timed region), TOP/s and fraction of the precision's dense MFMA
+             peak;
+  roofline   the dominant kernel (largest share of step time) against its
+             precision's MFMA peak, with HBM traffic from the committed
+             counter profile when it still matches the kernel sources;
+  cpu_baseline  the CPU oracle timed on this host on a bounded row sample of
+             the N = 8192 points, which also checks those GPU rows.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# Published dense (non-sparse) MFMA peaks of the MI355X, in T(FL)OP/s. INT4 runs
+# on the INT8 MFMA (gfx950 has no 4-bit integer MFMA), so its peak is INT8's.
+PEAK = {"f16": 2500.0, "s8": 5000.0, "s4": 5000.0}
+PEAK_UNIT = {"f16": "TFLOP/s", "s8": "TOP/s", "s4": "TOP/s"}
+IN_BYTES = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
+METRIC = "TFLOP/s | TOP/s at N=512–8192 for FP16, INT8, INT4; % of MFMA peak per dtype"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# rows of each N = 8192 point the CPU oracle computes for the baseline sample
+CPU_SAMPLE_ROWS = {"f16": 256, "s8": 1024, "s4": 1024}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    """Hash of the HIP sources, to tell whether stored counters still apply."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_10103_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(csrc, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def parse_points(spec: str):
+    import seeded_inputs as si
+    if spec == "sweep":
+        return si.sweep_points()
+    pts = []
+    sweep = {(d, n): s for d, n, s in si.sweep_points()}
+    for item in spec.split(","):
+        d, n = item.split(":")[:2]
+        n = int(n)
+        pts.append((d, n, sweep.get((d, n), 10)))
+    return pts
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--points", default="sweep",
+                    help='"sweep" or a list like "f16:8192,s8:4096"')
+    ap.add_argument("--variant", action="append", default=[],
+                    help="force a kernel variant for a point: dtype:N:variant")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_10103_amd as mp
+    import seeded_inputs as si
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    mp.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    props = torch.cuda.get_device_properties(dev)
+    forced = {}
+    for f in args.variant:
+        d, n, v = f.split(":")
+        forced[(d, int(n))] = int(v)
+
+    points = parse_points(args.points)
+    bufs = []
+    for dt, n, seed in points:
+        log(f"generating {dt} N={n} seed={seed}")
+        A, B = si.gen_operands(dt, n, n, n, seed=seed)
+        Ad = torch.from_numpy(A).to(dev)
+        Bd = torch.from_numpy(B).to(dev)
+        C = torch.empty((n, n), dtype=torch.float32 if dt == "f16" else torch.int32, device=dev)
+        v = forced.get((dt, n))
+        vsel = v if v is not None else mp.select_variant(dt, n, n, n, Ad.data_ptr(), Bd.data_ptr(),
+                                                         C.data_ptr())
+        bufs.append(dict(dt=dt, n=n, seed=seed, A=Ad, B=Bd, C=C, host=(A, B), variant=v,
+                         vname=mp.variant_name(dt, vsel)))
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.Stream(device=dev)  # default priority
+    fns = mp.GEMM
+
+    def step(events=None):
+        for i, b in enumerate(bufs):
+            if events is not None:
+                events[i][0].record(stream)
+            fns[b["dt"]](b["A"], b["B"], C=b["C"], stream=stream, variant=b["variant"])
+            if events is not None:
+                events[i][1].record(stream)
+
+    log(f"warmup {args.warmup} steps")
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            step()
+    torch.cuda.synchronize()
+
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in bufs] for _ in range(args.steps)]
+    log(f"timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        for s in range(args.steps):
+            step(evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    log(f"timed region {wall * 1e3:.1f} ms")
+
+    ms_per_step = wall * 1e3 / args.steps
+    total_ops = sum(2.0 * b["n"] ** 3 for b in bufs)
+    value = total_ops / (ms_per_step * 1e-3) / 1e12
+
+    pts = []
+    for i, b in enumerate(bufs):
+        ms = [evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)]
+        mean_ms = float(np.mean(ms))
+        ops = 2.0 * b["n"] ** 3
+        tops = ops / (mean_ms * 1e-3) / 1e12
+        pts.append(dict(dtype=b["dt"], n=b["n"], variant=b["vname"], ms=round(mean_ms, 5),
+                        ms_min=round(float(np.min(ms)), 5), ms_max=round(float(np.max(ms)), 5),
+                        tops=round(tops, 2), frac_peak=round(tops / PEAK[b["dt"]], 4),
+                        total_ms=mean_ms * args.steps))
+
+    dom = max(pts, key=lambda p: p["total_ms"])
+    n = dom["n"]
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        try:
+            tr = json.load(open(TRAFFIC_FILE))
+            key = f'{dom["dtype"]}:{n}:{dom["variant"]}'
+            ent = tr.get("points", {}).get(key)
+            if ent and tr.get("kernel_source_hash") == kernel_source_hash():
+                traffic = ent["hbm_bytes_per_launch"]
+        except (ValueError, KeyError, OSError):
+            traffic = None
+    roofline = dict(bound="mfma", kernel=f'{dom["dtype"]} N={n} {dom["variant"]}',
+                    achieved=round(dom["tops"], 2), peak=PEAK[dom["dtype"]],
+                    unit=PEAK_UNIT[dom["dtype"]], frac=round(dom["tops"] / PEAK[dom["dtype"]], 4),
+                    traffic=traffic,
+                    algorithmic_bytes=int((2 * IN_BYTES[dom["dtype"]] + 4) * n * n),
+                    algorithmic_ops=int(2 * n ** 3))
+    for p in pts:
+        p.pop("total_ms")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(bufs, log)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16->f32, s8->s32, s4->s32",
+        "data": "synthetic (seeded SplitMix64; FP16 U[-1,1], INT8 U{-128..127}, INT4 U{-8..7})",
+        "config": {
+            "workload": "precision x size sweep: square GEMM C=A*B (A row-major, B column-major), "
+                        "FP16/INT8/INT4 at N in {512,1024,2048,4096,8192}, seeds 10..24"
+                        if args.points == "sweep" else f"points {args.points}",
+            "points": len(bufs),
+            "ops_per_step": total_ops,
+        },
+        "device": {"name": props.name, "cus": props.multi_processor_count},
+        "points": pts,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(bufs, log):
+    """The CPU oracle, timed on this host's cores on a bounded row sample of
+    each N = 8192 point (or of the largest points present); its rows also
+    check the GPU output of those points."""
+    import oracle
+    import seeded_inputs as si
+    import torch
+
+    nmax = max(b["n"] for b in bufs)
+    big = [b for b in bufs if b["n"] == nmax]
+    threads = oracle.default_threads()
+    total_ops, total_s, checked, parts = 0.0, 0.0, True, []
+    for b in big:
+        dt, n = b["dt"], b["n"]
+        nrows = min(CPU_SAMPLE_ROWS[dt], n)
+        rows = si.sample_rows(b["seed"] + 2000, n, nrows, force=(0, n - 1))
+        A, B = b["host"]
+        log(f"cpu oracle {dt} N={n}: {len(rows)} rows on {threads} threads")
+        t0 = time.perf_counter()
+        if dt == "f16":
+            ref, D = oracle.gemm_f16(A, B, rows=rows, threads=threads)
+        elif dt == "s8":
+            ref, D = oracle.gemm_s8(A, B, rows=rows, threads=threads), None
+        else:
+            ref, D = oracle.gemm_s4(A, B, rows=rows, threads=threads), None
+        dt_s = time.perf_counter() - t0
+        ops = 2.0 * len(rows) * n * n
+        total_ops += ops
+        total_s += dt_s
+        got = b["C"][torch.from_numpy(rows.astype(np.int64)).to(b["C"].device)].cpu().numpy()
+        if dt == "f16":
+            ok = oracle.normalized_error(got, ref, D) <= 1e-3
+        else:
+            ok = bool(np.array_equal(got.astype(np.int64), ref))
+        checked = checked and ok
+        parts.append(f"{dt} N={n}: {len(rows)} rows in {dt_s:.2f} s")
+    try:
+        model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo")
+                     if l.startswith("model name"))
+    except (OSError, StopIteration):
+        model = "unknown"
+    return {
+        "value": round(total_ops / total_s / 1e12, 5),
+        "unit": "TOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": "; ".join(parts) + " (2*rows*N*N ops each)",
+        "cpu_model": model,
+        "cpu_count": os.cpu_count(),
+        "gpu_rows_match_oracle": checked,
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,109 @@
+/*
+ * mpgemm.h - dense C = A * B on one AMD Instinct MI355X (gfx950) in three
+ * precisions, on the matrix cores (MFMA).
+ *
+ * Operation (all three entry points). The paper's primitive is the matrix
+ * multiply-accumulate D = A*B + C (Background, "Tensor Cores, WMMA, and PTX
+ * mma.sync"); a GEMM starts from zero, so each call computes
+ *
+ *     C[i][j] = sum_{k=0}^{K-1} A(i,k) * B(k,j),   0 <= i < M, 0 <= j < N,
+ *
+ * and OVERWRITES C (no alpha/beta, no accumulation into C's old contents).
+ *
+ * Layouts (the ".row.col" operand order of the paper's INT4 MMA, Listing
+ * "lst:int4-primitives"; the layouts of the paper's tiles in Listings
+ * "lst:int4-double-buffer" and "lst:int4-three-stage"): dense, no leading
+ * dimensions.
+ *   A  row-major M x K:     A(i,k) at element i*K + k.
+ *   B  column-major K x N:  B(k,j) at element j*K + k (N rows of K).
+ *   C  row-major M x N:     C[i][j] at element i*N + j.
+ *
+ * Memory and ownership. A, B and C are DEVICE pointers on the current HIP
+ * device, owned by the caller; the library never allocates, frees or copies
+ * them and keeps no pointer after the call returns. C must not overlap A or B.
+ * Any alignment is accepted; 16-byte aligned operands whose shapes match a
+ * tuned tile take the fast kernels, everything else a bounds-checked kernel.
+ *
+ * Streams. Work is enqueued on `stream` (0 = the null stream) and the call
+ * returns without synchronising. Calls on different streams may run
+ * concurrently; the library holds no mutable state shared between calls.
+ * Faults inside a kernel surface at the caller's next synchronisation of the
+ * stream, not in the return value.
+ *
+ * Errors. Each entry point returns hipSuccess or:
+ *   hipErrorInvalidValue  M, N or K negative; K odd for INT4; a required
+ *                         pointer NULL (A and B when M, N, K > 0; C when
+ *                         M, N > 0); C overlapping A or B; a problem whose
+ *                         element counts overflow 64-bit byte offsets;
+ *   the launch error      if the kernel launch itself fails.
+ * Nothing is enqueued when an argument error is returned.
+ * Degenerate sizes: M == 0 or N == 0 is a no-op returning hipSuccess; K == 0
+ * writes zeros to C (empty sums).
+ */
+#ifndef MPGEMM_H
+#define MPGEMM_H
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* FP16 inputs, FP32 accumulation and output (paper Run 1; Table VI lists the
+ * f32-accumulator FP16 kernels). A and B hold IEEE binary16 values (finite or
+ * not: the hardware's IEEE arithmetic decides inf/NaN propagation); C receives
+ * binary32. Products are summed in FP32 in an unspecified order, so results
+ * are not bit-unique; the library's tests bound them by
+ * |C - exact| <= 1e-3 * sum_k |A(i,k)| |B(k,j)|. */
+hipError_t gemm_f16_f32(int M, int N, int K, const void *A, const void *B, float *C,
+                        hipStream_t stream);
+
+/* Signed INT8 inputs, INT32 accumulation and output (paper Run 2). Exact: C
+ * equals the integer sum whenever every partial sum fits in int32, which
+ * always holds for K < 131072 (|a*b| <= 2^14); results beyond that range are
+ * not specified. */
+hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, int32_t *C,
+                       hipStream_t stream);
+
+/* Signed INT4 inputs, INT32 accumulation and output (paper Run 3: the
+ * ".s4.s4.s32" MMA, no dequantisation or scaling). K must be even. Values are
+ * two's-complement nibbles packed two per byte along K, the low nibble holding
+ * the even k: A is M rows of K/2 bytes, B is N rows of K/2 bytes. Exact
+ * whenever every partial sum fits in int32, which always holds for K < 2^25
+ * (|a*b| <= 64). */
+hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
+                       hipStream_t stream);
+
+/* ---- introspection and tuning (same operation, explicit kernel choice) ----
+ * dtype: 0 = FP16->FP32, 1 = INT8->INT32, 2 = INT4->INT32. A variant is one
+ * compiled kernel configuration (tile shape, wave layout, pipeline depth).
+ * Variant 0 of every dtype is the bounds-checked kernel that accepts any
+ * shape and alignment. */
+
+/* Number of variants for dtype, or -1 for an unknown dtype. */
+int mpgemm_num_variants(int dtype);
+
+/* Static, NUL-terminated name of a variant ("" if out of range). */
+const char *mpgemm_variant_name(int dtype, int variant);
+
+/* The variant the dtype's entry point runs for these arguments (pointers are
+ * only inspected for alignment), or -1 if the arguments are invalid. */
+int mpgemm_select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
+                          const void *C);
+
+/* Whether `variant` can run these arguments: 1 yes, 0 no, -1 invalid dtype. */
+int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const void *A,
+                            const void *B, const void *C);
+
+/* Run one specific variant with the same semantics, validation and errors as
+ * the dtype's entry point; hipErrorInvalidValue also when the variant does not
+ * support the arguments. C is float* for dtype 0, int32_t* otherwise. */
+hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const void *A,
+                              const void *B, void *C, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MPGEMM_H */

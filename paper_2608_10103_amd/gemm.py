@@ -1,0 +1,175 @@
+"""Python binding for libmpgemm.so (the C ABI in include/mpgemm.h).
+
+Argument marshalling only: shape/dtype/device checks, then a ctypes call into
+the HIP library, which validates again and enqueues its own kernels on the
+given stream. PyTorch supplies device memory and streams; no torch operator
+runs on the GPU path. If the library is not built this module raises instead
+of computing anything another way.
+
+Operand conventions (see include/mpgemm.h):
+  A  (M, K)    row-major          float16 / int8, or uint8 (M, K/2) for INT4
+  B  (N, K)    = K x N column-major, same dtypes (uint8 (N, K/2) for INT4)
+  C  (M, N)    row-major          float32 (FP16 path) or int32
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmpgemm.so")
+DTYPE_CODE = {"f16": 0, "s8": 1, "s4": 2}
+_IN_DTYPE = {"f16": torch.float16, "s8": torch.int8, "s4": torch.uint8}
+_OUT_DTYPE = {"f16": torch.float32, "s8": torch.int32, "s4": torch.int32}
+_lib = None
+
+
+class HipError(RuntimeError):
+    """A non-zero hipError_t returned by the library."""
+
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: hipError_t {code}")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                           "or python -m paper_2608_10103_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    I, P = ctypes.c_int, ctypes.c_void_p
+    for name in ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32"):
+        fn = getattr(L, name)
+        fn.argtypes = [I, I, I, P, P, P, P]
+        fn.restype = I
+    L.mpgemm_num_variants.argtypes = [I]
+    L.mpgemm_num_variants.restype = I
+    L.mpgemm_variant_name.argtypes = [I, I]
+    L.mpgemm_variant_name.restype = ctypes.c_char_p
+    L.mpgemm_select_variant.argtypes = [I, I, I, I, P, P, P]
+    L.mpgemm_select_variant.restype = I
+    L.mpgemm_variant_supports.argtypes = [I, I, I, I, I, P, P, P]
+    L.mpgemm_variant_supports.restype = I
+    L.mpgemm_run_variant.argtypes = [I, I, I, I, I, P, P, P, P]
+    L.mpgemm_run_variant.restype = I
+    _lib = L
+    return L
+
+
+EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
+                    "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
+                    "mpgemm_run_variant")
+
+
+def _stream_ptr(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return int(stream.cuda_stream)
+
+
+def _shapes(dtype: str, A: torch.Tensor, B: torch.Tensor):
+    want = _IN_DTYPE[dtype]
+    for name, t in (("A", A), ("B", B)):
+        if not isinstance(t, torch.Tensor) or t.dtype != want or t.dim() != 2:
+            raise TypeError(f"{name} must be a 2-D {want} tensor")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on a GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if A.device != B.device:
+        raise ValueError("A and B must be on the same device")
+    M, KA = A.shape
+    N, KB = B.shape
+    if KA != KB:
+        raise ValueError(f"K mismatch: A has {KA}, B has {KB} per row")
+    K = 2 * KA if dtype == "s4" else KA
+    return M, N, K
+
+
+def _out(dtype, M, N, A, C):
+    if C is None:
+        return torch.empty((M, N), dtype=_OUT_DTYPE[dtype], device=A.device)
+    if C.dtype != _OUT_DTYPE[dtype] or tuple(C.shape) != (M, N) or not C.is_contiguous():
+        raise ValueError(f"C must be a contiguous ({M}, {N}) {_OUT_DTYPE[dtype]} tensor")
+    if C.device != A.device:
+        raise ValueError("C must be on the operands' device")
+    return C
+
+
+def _call(dtype: str, A, B, C, stream, variant):
+    M, N, K = _shapes(dtype, A, B)
+    C = _out(dtype, M, N, A, C)
+    s = _stream_ptr(stream, A.device)
+    with torch.cuda.device(A.device):
+        if variant is None:
+            fn = getattr(lib(), {"f16": "gemm_f16_f32", "s8": "gemm_s8_s32",
+                                 "s4": "gemm_s4_s32"}[dtype])
+            code = fn(M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
+        else:
+            code = lib().mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, A.data_ptr(),
+                                            B.data_ptr(), C.data_ptr(), s)
+    if code != 0:
+        raise HipError(code, f"{dtype} GEMM {M}x{N}x{K}")
+    return C
+
+
+def gemm_f16_f32(A, B, C=None, stream=None, variant=None):
+    """C = A @ B with FP16 A (M, K), FP16 B (N, K) = K x N column-major; FP32 C."""
+    return _call("f16", A, B, C, stream, variant)
+
+
+def gemm_s8_s32(A, B, C=None, stream=None, variant=None):
+    """C = A @ B with INT8 A (M, K), INT8 B (N, K); INT32 C."""
+    return _call("s8", A, B, C, stream, variant)
+
+
+def gemm_s4_s32(A, B, C=None, stream=None, variant=None):
+    """C = A @ B with packed INT4 A (M, K/2) and B (N, K/2) uint8 (low nibble =
+    even k); INT32 C."""
+    return _call("s4", A, B, C, stream, variant)
+
+
+GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
+
+
+def raw_call(dtype: str, M: int, N: int, K: int, a_ptr: int, b_ptr: int, c_ptr: int,
+             stream_ptr: int = 0, variant: int | None = None) -> int:
+    """Call an entry point with raw integers/pointers; returns the hipError_t."""
+    L = lib()
+    if variant is None:
+        fn = getattr(L, {"f16": "gemm_f16_f32", "s8": "gemm_s8_s32", "s4": "gemm_s4_s32"}[dtype])
+        return fn(M, N, K, a_ptr, b_ptr, c_ptr, stream_ptr)
+    return L.mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, a_ptr, b_ptr, c_ptr,
+                                stream_ptr)
+
+
+def num_variants(dtype: str) -> int:
+    return lib().mpgemm_num_variants(DTYPE_CODE[dtype])
+
+
+def variant_name(dtype: str, variant: int) -> str:
+    return lib().mpgemm_variant_name(DTYPE_CODE[dtype], variant).decode()
+
+
+def select_variant(dtype: str, M: int, N: int, K: int, a_ptr: int = 0, b_ptr: int = 0,
+                   c_ptr: int = 16) -> int:
+    """Variant the entry point would run (pointers only matter for alignment;
+    the defaults are 16-byte aligned stand-ins, never dereferenced)."""
+    if a_ptr == 0:
+        a_ptr = 1 << 20
+    if b_ptr == 0:
+        b_ptr = 1 << 40
+    if c_ptr == 16:
+        c_ptr = 1 << 44
+    return lib().mpgemm_select_variant(DTYPE_CODE[dtype], M, N, K, a_ptr, b_ptr, c_ptr)
+
+
+def variant_supports(dtype: str, variant: int, M: int, N: int, K: int, a_ptr: int = 1 << 20,
+                     b_ptr: int = 1 << 40, c_ptr: int = 1 << 44) -> bool:
+    return lib().mpgemm_variant_supports(DTYPE_CODE[dtype], variant, M, N, K, a_ptr, b_ptr,
+                                         c_ptr) == 1

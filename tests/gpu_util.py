@@ -1,0 +1,47 @@
+"""Helpers for the GPU tests: move seeded numpy operands to the GPU, run one
+entry point through the C ABI, and compare with the oracle."""
+import numpy as np
+import torch
+
+import oracle
+import paper_2608_10103_amd as mp
+
+TORCH_IN = {"f16": torch.float16, "s8": torch.int8, "s4": torch.uint8}
+F16_TOL = 1e-3  # max |C_gpu - C_exact| / sum_k |a||b|
+
+
+def dev(x: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda")
+
+
+def gpu_gemm(dtype, A, B, variant=None, stream=None):
+    """Run the dtype's entry point (or a given variant) on numpy operands;
+    returns C as numpy (float32 or int32)."""
+    Ad, Bd = dev(A), dev(B)
+    C = mp.GEMM[dtype](Ad, Bd, variant=variant, stream=stream)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+def oracle_gemm(dtype, A, B, rows=None):
+    """(C_ref, D) where D is the FP16 error scale (None for integers)."""
+    if dtype == "f16":
+        return oracle.gemm_f16(A, B, rows=rows)
+    if dtype == "s8":
+        return oracle.gemm_s8(A, B, rows=rows), None
+    return oracle.gemm_s4(A, B, rows=rows), None
+
+
+def assert_parity(dtype, C_gpu, C_ref, D, what=""):
+    """Bit-exact for the integer paths, normalised error <= 1e-3 for FP16."""
+    if dtype == "f16":
+        assert C_gpu.dtype == np.float32
+        err = oracle.normalized_error(C_gpu, C_ref, D)
+        assert err <= F16_TOL, f"{what}: normalised error {err:.3e} > {F16_TOL}"
+        return err
+    assert C_gpu.dtype == np.int32
+    assert np.all(np.abs(C_ref) < 2**31), f"{what}: oracle result leaves int32"
+    bad = np.argwhere(C_gpu.astype(np.int64) != C_ref)
+    assert bad.size == 0, (f"{what}: {len(bad)} mismatches, first at {tuple(bad[0])}: "
+                           f"gpu {C_gpu[tuple(bad[0])]} oracle {C_ref[tuple(bad[0])]}")
+    return 0.0

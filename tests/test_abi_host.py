@@ -1,0 +1,94 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/mpgemm.h declares, and its argument checks and kernel
+choice behave as documented (these entry points never touch the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_10103_amd as mp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mpgemm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32"} <= set(names)
+    lib = ctypes.CDLL(mp.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in mpgemm.h but not exported"
+    assert set(names) == set(mp.EXPORTED_SYMBOLS)
+
+
+def test_variant_table():
+    for dt in ("f16", "s8", "s4"):
+        n = mp.num_variants(dt)
+        assert n >= 2
+        assert mp.variant_name(dt, 0).startswith("generic")
+        assert all(mp.variant_name(dt, v).startswith("tile") for v in range(1, n))
+        assert mp.variant_name(dt, n) == ""
+    assert mp.lib().mpgemm_num_variants(7) == -1
+
+
+@pytest.mark.parametrize("dt", ["f16", "s8", "s4"])
+@pytest.mark.parametrize("n", [512, 1024, 2048, 4096, 8192])
+def test_sweep_sizes_take_tiled_kernels(dt, n):
+    v = mp.select_variant(dt, n, n, n)
+    assert v > 0, f"{dt} {n} falls back to the bounds-checked kernel"
+
+
+def test_selection_falls_back_when_needed():
+    assert mp.select_variant("s8", 1000, 1024, 1024) == 0  # M off the tile grid
+    assert mp.select_variant("s8", 1024, 1024, 1000) == 0  # K off the K-slice
+    assert mp.select_variant("s8", 1024, 1024, 1024, a_ptr=(1 << 20) + 4) == 0  # unaligned A
+    assert mp.select_variant("s4", 256, 256, 262144) == 0  # scaled INT4 range exceeded
+    assert mp.select_variant("s4", 256, 256, 0) == 0       # K = 0: zero fill
+
+
+def test_invalid_arguments_rejected_on_host():
+    L = mp.lib()
+    sel = lambda dt, M, N, K, a=1 << 20, b=1 << 40, c=1 << 44: L.mpgemm_select_variant(dt, M, N, K, a, b, c)
+    assert sel(1, -1, 8, 8) == -1
+    assert sel(2, 8, 8, 7) == -1                 # odd K for INT4
+    assert sel(1, 8, 8, 8, a=0) == -1            # NULL A
+    assert sel(1, 8, 8, 8, c=0) == -1            # NULL C
+    assert sel(1, 8, 8, 8, c=(1 << 44) + 2) == -1  # C not 4-byte aligned
+    assert sel(0, 8, 8, 8, a=(1 << 20) + 1) == -1  # FP16 A not 2-byte aligned
+    assert sel(1, 8, 8, 8, c=(1 << 20) + 16) == -1  # C overlaps A
+    assert sel(5, 8, 8, 8) == -1                 # unknown dtype
+    assert sel(1, 0, 8, 8, a=0, b=0, c=0) == 0   # empty: valid no-op
+    assert L.mpgemm_variant_supports(9, 0, 8, 8, 8, 1 << 20, 1 << 40, 1 << 44) == -1
+    assert L.mpgemm_run_variant(1, -1, 8, 8, 8, 1 << 20, 1 << 40, 1 << 44, None) != 0
+
+
+def _swz(ch, q):
+    # the LDS chunk swizzle of device_common.hpp (swz<CH>)
+    if ch == 8:
+        return (q ^ (q >> 3)) & 7
+    return ((q >> 1) ^ (q >> 3)) & 3
+
+
+@pytest.mark.parametrize("ch", [8, 4])
+def test_lds_swizzle_is_conflict_free(ch):
+    """An MFMA operand fetch reads chunk c of 32 consecutive LDS rows (16 bytes
+    each). In 8-lane groups (128 bytes per cycle) and in 16-lane groups (256
+    bytes per cycle) every lane must hit a different 16-byte bank group."""
+    row_bytes = 16 * ch
+    for base in range(0, 256, 32):
+        for c in range(ch):
+            addrs = [(base + r) * row_bytes + 16 * (c ^ _swz(ch, base + r)) for r in range(32)]
+            for group, width in ((8, 128), (16, 256)):
+                for g0 in range(0, 32, group):
+                    slots = {(a % width) // 16 for a in addrs[g0:g0 + group]}
+                    assert len(slots) == group, (ch, base, c, group)
+    # and the swizzle is a permutation of the chunks of every row
+    for q in range(64):
+        assert sorted(c ^ _swz(ch, q) for c in range(ch)) == list(range(ch))

@@ -1,0 +1,317 @@
+"""GPU parity: the HIP library through its C ABI against the CPU oracle.
+
+Workloads: the five named configurations (FP16 512 uniform seed 0; INT8 2048
+seed 1; INT4 4096 seed 2; FP16 8192 normal seed 3 on 256 sampled rows plus the
+first and last; the 15-point precision x size sweep, seeds 10..24), every
+compiled kernel variant on shapes spanning several tiles, closed forms and
+edge cases. Integer results must match bit for bit; FP16 within a normalised
+error of 1e-3.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_10103_amd as mp
+import seeded_inputs as si
+from tests.gpu_util import F16_TOL, assert_parity, dev, gpu_gemm, oracle_gemm
+
+pytestmark = pytest.mark.gpu
+
+DTYPES = ("f16", "s8", "s4")
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+# ---------------------------------------------------------------- named configurations
+
+
+def test_f16_512_first_launch():
+    """FP16 512^3, U[-1,1] seed 0, full oracle, the very first launch."""
+    A, B = si.gen_operands("f16", 512, 512, 512, seed=0, dist="uniform")
+    C = gpu_gemm("f16", A, B)
+    ref, D = oracle_gemm("f16", A, B)
+    err = assert_parity("f16", C, ref, D, "f16 512")
+    _log(f"f16 512 normalised error {err:.3e}")
+
+
+def test_s8_2048():
+    A, B = si.gen_operands("s8", 2048, 2048, 2048, seed=1)
+    assert_parity("s8", gpu_gemm("s8", A, B), *oracle_gemm("s8", A, B), "s8 2048")
+
+
+def test_s4_4096():
+    A, B = si.gen_operands("s4", 4096, 4096, 4096, seed=2)
+    assert_parity("s4", gpu_gemm("s4", A, B), *oracle_gemm("s4", A, B), "s4 4096")
+
+
+def test_f16_8192_sampled_rows():
+    n = 8192
+    A, B = si.gen_operands("f16", n, n, n, seed=3, dist="normal")
+    C = gpu_gemm("f16", A, B)
+    rows = si.sample_rows(si.F16_8192_ROW_SEED, n, si.F16_8192_ROW_COUNT, force=(0, n - 1))
+    ref, D = oracle_gemm("f16", A, B, rows=rows)
+    err = assert_parity("f16", C[rows], ref, D, "f16 8192 rows")
+    _log(f"f16 8192 ({len(rows)} rows) normalised error {err:.3e}")
+
+
+def test_f16_8192_all_ones_and_identity():
+    n = 8192
+    ones = torch.ones((n, n), dtype=torch.float16, device="cuda")
+    C = mp.gemm_f16_f32(ones, ones)
+    torch.cuda.synchronize()
+    assert bool((C == float(n)).all())
+    del C
+    # identity: A = I, so C = B read as a K x N matrix (B stored (N, K) -> C = B^T)
+    _, B = si.gen_operands("f16", 1, n, n, seed=3, dist="normal")
+    eye = torch.eye(n, dtype=torch.float16, device="cuda")
+    C = mp.gemm_f16_f32(eye, dev(B)).cpu().numpy()
+    want = B.T.astype(np.float32)
+    sub = np.abs(B.T.astype(np.float64)) < 2.0 ** -14  # binary16 subnormals (and zeros)
+    assert np.array_equal(C[~sub], want[~sub])
+    ok = (C[sub] == want[sub]) | (C[sub] == 0)
+    assert ok.all()
+    kept = int(np.sum((C[sub] == want[sub]) & (want[sub] != 0)))
+    _log(f"identity 8192: {int(sub.sum())} subnormal/zero inputs, {kept} nonzero subnormals kept exactly")
+
+
+SWEEP = si.sweep_points()
+
+
+@pytest.mark.parametrize("dtype,n,seed", SWEEP, ids=[f"{d}-{n}" for d, n, _ in SWEEP])
+def test_sweep_point(dtype, n, seed):
+    """Precision x size sweep. INT8/INT4 in full at every size; FP16 in full up
+    to 4096 and on the sampled-row protocol at 8192."""
+    A, B = si.gen_operands(dtype, n, n, n, seed=seed)
+    C = gpu_gemm(dtype, A, B)
+    rows = None
+    if dtype == "f16" and n == 8192:
+        rows = si.sample_rows(seed + 1000, n, 256, force=(0, n - 1))
+    ref, D = oracle_gemm(dtype, A, B, rows=rows)
+    got = C if rows is None else C[rows]
+    err = assert_parity(dtype, got, ref, D, f"{dtype} {n}")
+    _log(f"sweep {dtype} {n} seed {seed}: ok (err {err:.2e}), variant "
+         f"{mp.variant_name(dtype, mp.select_variant(dtype, n, n, n))}")
+
+
+# ---------------------------------------------------------------- every variant
+
+
+def _variant_shapes(dtype, v):
+    """Shapes a variant supports that span several tiles and K-slices."""
+    name = mp.variant_name(dtype, v)
+    if name.startswith("generic"):
+        return [(97, 65, 130), (33, 31, 66)]
+    tile = name.split("_")[0][len("tile"):]
+    bm, bn = (int(x) for x in tile.split("x"))
+    kb = int(name.split("_k")[1].split("_")[0])
+    elems_per_kb = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
+    return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb)]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_every_variant(dtype):
+    for v in range(mp.num_variants(dtype)):
+        for (M, N, K) in _variant_shapes(dtype, v):
+            assert mp.variant_supports(dtype, v, M, N, K)
+            A, B = si.gen_operands(dtype, M, N, K, seed=1000 + v)
+            C = gpu_gemm(dtype, A, B, variant=v)
+            assert_parity(dtype, C, *oracle_gemm(dtype, A, B),
+                          f"{dtype} variant {mp.variant_name(dtype, v)} {M}x{N}x{K}")
+        _log(f"{dtype} variant {mp.variant_name(dtype, v)}: ok")
+
+
+# ---------------------------------------------------------------- closed forms
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_all_ones_closed_form(dtype):
+    for n in (512, 4096):
+        kw = n // 2 if dtype == "s4" else n
+        fill = {"f16": 1.0, "s8": 1, "s4": 0x11}[dtype]
+        t = torch.full((n, kw), fill, dtype={"f16": torch.float16, "s8": torch.int8,
+                                            "s4": torch.uint8}[dtype], device="cuda")
+        C = mp.GEMM[dtype](t, t)
+        torch.cuda.synchronize()
+        assert bool((C == n).all()), f"{dtype} all-ones {n}"
+
+
+def test_integer_extremes():
+    K = 8192
+    m = torch.full((256, K), -128, dtype=torch.int8, device="cuda")
+    C = mp.gemm_s8_s32(m, m)
+    assert bool((C == 16384 * K).all())  # 2^27, the int32 headroom case
+    p = torch.full((256, K), 127, dtype=torch.int8, device="cuda")
+    assert bool((mp.gemm_s8_s32(m, p) == -16256 * K).all())
+    e4 = torch.full((256, K // 2), 0x88, dtype=torch.uint8, device="cuda")  # all -8
+    assert bool((mp.gemm_s4_s32(e4, e4) == 64 * K).all())
+    s4 = torch.full((256, K // 2), 0x77, dtype=torch.uint8, device="cuda")  # all 7
+    assert bool((mp.gemm_s4_s32(e4, s4) == -56 * K).all())
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", ["s8", "s4"])
+def test_permutation(dtype):
+    """A = P (a permutation matrix): row i of C is column perm[i] of B."""
+    K = N = 1024
+    perm = np.random.default_rng(7).permutation(K)
+    P = np.zeros((K, K), np.int8)
+    P[np.arange(K), perm] = 1
+    _, B = si.gen_operands(dtype, 1, N, K, seed=5)
+    A = P if dtype == "s8" else si.pack_s4(P)
+    C = gpu_gemm(dtype, A, B)
+    Bl = B.astype(np.int64) if dtype == "s8" else oracle.s4_unpack(B).astype(np.int64)
+    assert np.array_equal(C.astype(np.int64), Bl.T[perm])
+
+
+def test_s4_every_nibble_through_the_api():
+    """A = I (packed) and B cycling through all 256 byte values: C = B, so every
+    nibble decode of the B side shows up in C; then the roles swapped."""
+    K = 512
+    I = si.pack_s4(np.eye(K, dtype=np.int8))
+    Bb = (np.arange(256 * (K // 2)) % 256).astype(np.uint8).reshape(256, K // 2)
+    Bb = np.ascontiguousarray(np.roll(Bb, 3, axis=1))
+    want = np.empty((256, K), np.int64)
+    lo, hi = (Bb & 0xF).astype(np.int64), (Bb >> 4).astype(np.int64)
+    want[:, 0::2] = np.where(lo >= 8, lo - 16, lo)
+    want[:, 1::2] = np.where(hi >= 8, hi - 16, hi)
+    C = gpu_gemm("s4", I, Bb)  # (K, 256): C[k, j] = B(k, j)
+    assert np.array_equal(C.astype(np.int64), want.T)
+    C2 = gpu_gemm("s4", Bb, I)  # (256, K): C[i, k] = A(i, k)
+    assert np.array_equal(C2.astype(np.int64), want)
+
+
+@pytest.mark.parametrize("n", [512, 4096])
+def test_f16_small_integers_bit_exact(n):
+    """Integer-valued FP16 inputs with |v| <= 8: every partial sum is an integer
+    below 2^24, so FP32 accumulation is exact in any order."""
+    w = si.splitmix64(77, 0, 2 * n * n)
+    vals = (si.words_to_int8(w).astype(np.int16) // 16).astype(np.float16)  # [-8, 7]
+    A, B = vals[:n * n].reshape(n, n), vals[n * n:].reshape(n, n)
+    C = gpu_gemm("f16", A, B)
+    ref = A.astype(np.int64) @ B.astype(np.int64).T
+    assert np.array_equal(C.astype(np.int64), ref)
+
+
+# ---------------------------------------------------------------- edge cases
+
+
+EDGE = [1, 2, 3, 31, 33, 100]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_edge_shapes(dtype):
+    for M in EDGE:
+        for N in EDGE:
+            for K in (1, 2, 3, 31, 33, 100):
+                if dtype == "s4" and K % 2:
+                    continue
+                A, B = si.gen_operands(dtype, M, N, K, seed=M * 10007 + N * 101 + K)
+                C = gpu_gemm(dtype, A, B)
+                assert_parity(dtype, C, *oracle_gemm(dtype, A, B), f"{dtype} {M}x{N}x{K}")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_ragged_large(dtype):
+    """Sizes just off the tile grid go to the bounds-checked kernel."""
+    M, N, K = 1000, 777, 1030
+    A, B = si.gen_operands(dtype, M, N, K, seed=4242)
+    assert mp.select_variant(dtype, M, N, K) == 0
+    assert_parity(dtype, gpu_gemm(dtype, A, B), *oracle_gemm(dtype, A, B), f"{dtype} ragged")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_k_zero_writes_zeros(dtype):
+    M, N = 70, 40
+    C = torch.full((M, N), 7, dtype=torch.float32 if dtype == "f16" else torch.int32,
+                   device="cuda")
+    kw = 0
+    A = torch.empty((M, kw), dtype={"f16": torch.float16, "s8": torch.int8,
+                                    "s4": torch.uint8}[dtype], device="cuda")
+    B = torch.empty((N, kw), dtype=A.dtype, device="cuda")
+    mp.GEMM[dtype](A, B, C=C)
+    torch.cuda.synchronize()
+    assert bool((C == 0).all())
+
+
+def test_empty_m_or_n_is_noop():
+    assert mp.raw_call("s8", 0, 5, 8, 0, 0, 0) == 0
+    assert mp.raw_call("f16", 5, 0, 8, 0, 0, 0) == 0
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_unaligned_operands(dtype):
+    """Operands offset from 16-byte alignment (element-aligned) take the
+    bounds-checked kernel and stay exact."""
+    M, N, K = 256, 256, 256
+    A, B = si.gen_operands(dtype, M, N, K, seed=99)
+    esz = 2 if dtype == "f16" else 1
+    kw = A.shape[1]
+    raw = torch.empty(M * kw * esz + 64, dtype=torch.uint8, device="cuda")
+    rawb = torch.empty(N * kw * esz + 64, dtype=torch.uint8, device="cuda")
+    off = esz  # one element past a 16-byte boundary
+    raw[off:off + A.nbytes].copy_(torch.from_numpy(A.view(np.uint8).ravel()).cuda())
+    rawb[off:off + B.nbytes].copy_(torch.from_numpy(B.view(np.uint8).ravel()).cuda())
+    C = torch.empty((M, N), dtype=torch.float32 if dtype == "f16" else torch.int32, device="cuda")
+    a_ptr, b_ptr = raw.data_ptr() + off, rawb.data_ptr() + off
+    assert mp.lib().mpgemm_select_variant(mp.gemm.DTYPE_CODE[dtype], M, N, K, a_ptr, b_ptr,
+                                          C.data_ptr()) == 0
+    code = mp.raw_call(dtype, M, N, K, a_ptr, b_ptr, C.data_ptr(),
+                       torch.cuda.current_stream().cuda_stream)
+    assert code == 0
+    torch.cuda.synchronize()
+    assert_parity(dtype, C.cpu().numpy(), *oracle_gemm(dtype, A, B), f"{dtype} unaligned")
+
+
+def test_argument_errors():
+    a = torch.zeros((64, 64), dtype=torch.int8, device="cuda")
+    c = torch.zeros((64, 64), dtype=torch.int32, device="cuda")
+    pa, pc = a.data_ptr(), c.data_ptr()
+    INVALID = 1  # hipErrorInvalidValue
+    assert mp.raw_call("s8", -1, 64, 64, pa, pa, pc) == INVALID
+    assert mp.raw_call("s8", 64, 64, -2, pa, pa, pc) == INVALID
+    assert mp.raw_call("s4", 64, 64, 63, pa, pa, pc) == INVALID  # odd K
+    assert mp.raw_call("s8", 64, 64, 64, 0, pa, pc) == INVALID
+    assert mp.raw_call("s8", 64, 64, 64, pa, pa, 0) == INVALID
+    assert mp.raw_call("s8", 64, 64, 64, pa, pa, pa) == INVALID  # C overlaps A
+    assert mp.raw_call("s8", 64, 64, 64, pa, pa, pc + 2) == INVALID  # C misaligned
+    h = torch.zeros((64, 64), dtype=torch.float16, device="cuda")
+    assert mp.raw_call("f16", 64, 64, 64, h.data_ptr() + 1, h.data_ptr(), pc) == INVALID
+    assert mp.raw_call("s8", 64, 64, 64, pa, pa, pc, variant=99) == INVALID
+    # a tiled variant refuses shapes off its tile grid
+    assert mp.raw_call("s8", 100, 256, 256, pa, pa, pc, variant=1) == INVALID
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- determinism and streams
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_repeat_launches_identical(dtype):
+    n = 2048
+    A, B = si.gen_operands(dtype, n, n, n, seed=31)
+    Ad, Bd = dev(A), dev(B)
+    first = mp.GEMM[dtype](Ad, Bd)
+    for _ in range(4):
+        again = mp.GEMM[dtype](Ad, Bd)
+        torch.cuda.synchronize()
+        assert torch.equal(first, again)
+
+
+def test_two_streams():
+    n = 1024
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    A, B = si.gen_operands("s8", n, n, n, seed=41)
+    A2, B2 = si.gen_operands("s4", n, n, n, seed=42)
+    Ad, Bd, A2d, B2d = dev(A), dev(B), dev(A2), dev(B2)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        C1 = mp.gemm_s8_s32(Ad, Bd, stream=s1)
+    with torch.cuda.stream(s2):
+        C2 = mp.gemm_s4_s32(A2d, B2d, stream=s2)
+    s1.synchronize()
+    s2.synchronize()
+    assert_parity("s8", C1.cpu().numpy(), *oracle_gemm("s8", A, B), "stream 1")
+    assert_parity("s4", C2.cpu().numpy(), *oracle_gemm("s4", A2, B2), "stream 2")
