@@ -20,6 +20,15 @@ namespace mpg {
 //                BM   BN  WGM WGN BKB STG GROUP_M
 typedef TileCfg<256, 256, 2, 2, 128, 2, 4> T256x256_w4_s2;
 typedef TileCfg<256, 256, 2, 4, 128, 2, 4> T256x256_w8_s2;
+typedef TileCfg<256, 256, 4, 2, 128, 2, 4> T256x256_w8t_s2;
+typedef TileCfg<256, 256, 4, 4, 128, 2, 4> T256x256_w16_s2;
+typedef TileCfg<256, 256, 4, 2, 64, 4, 4> T256x256_w8t_k64_s4;
+typedef TileCfg<256, 256, 4, 4, 64, 4, 4> T256x256_w16_k64_s4;
+typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4b;
+typedef TileCfg<128, 128, 2, 2, 64, 4, 4> T128x128_w4_k64_s4;
+typedef TileCfg<256, 256, 2, 2, 64, 2, 4> T256x256_w4_k64_s2;
+typedef TileCfg<256, 256, 4, 2, 64, 2, 4> T256x256_w8t_k64_s2;
+typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_k128_s2;
 typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4;
 typedef TileCfg<256, 128, 2, 2, 128, 3, 4> T256x128_w4_s3;
 typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
@@ -49,6 +58,18 @@ Variant tiled(const char *name) {
     return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
 }
 
+template <int DT, class T, bool SPREAD = false>
+Variant pipelined(const char *name) {
+    kernel_fn f = &tiled_gemm_pf<DT, T, SPREAD>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+}
+
+template <int DT, class T, int NSETS>
+Variant staged(const char *name) {
+    kernel_fn f = &tiled_gemm_rs<DT, T, NSETS>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+}
+
 template <int DT>
 Variant generic(const char *name) {
     generic_fn f = &generic_gemm<DT>;
@@ -63,7 +84,28 @@ Variant generic(const char *name) {
      tiled<DT, T256x128_w4_s3>("tile256x128_w2x2_k128_s3"),                \
      tiled<DT, T128x128_w4_s2>("tile128x128_w2x2_k128_s2"),                \
      tiled<DT, T128x128_w4_s4>("tile128x128_w2x2_k128_s4"),                \
-     tiled<DT, T64x64_w1_s4>("tile64x64_w1x1_k128_s4")}
+     tiled<DT, T64x64_w1_s4>("tile64x64_w1x1_k128_s4"),                    \
+     pipelined<DT, T256x256_w4_s2>("pipe256x256_w2x2_k128_s2"),            \
+     pipelined<DT, T256x256_w8_s2>("pipe256x256_w2x4_k128_s2"),            \
+     pipelined<DT, T256x256_w4_k64_s4>("pipe256x256_w2x2_k64_s4"),         \
+     pipelined<DT, T256x128_w4_s3>("pipe256x128_w2x2_k128_s3"),            \
+     pipelined<DT, T128x128_w4_s4>("pipe128x128_w2x2_k128_s4"),            \
+     pipelined<DT, T64x64_w1_s4>("pipe64x64_w1x1_k128_s4"),                \
+     pipelined<DT, T256x256_w8t_s2>("pipe256x256_w4x2_k128_s2"),           \
+     pipelined<DT, T256x256_w16_s2>("pipe256x256_w4x4_k128_s2"),           \
+     pipelined<DT, T256x256_w8t_k64_s4, true>("spread256x256_w4x2_k64_s4"), \
+     pipelined<DT, T256x256_w8t_s2, true>("spread256x256_w4x2_k128_s2"),   \
+     pipelined<DT, T256x256_w16_k64_s4, true>("spread256x256_w4x4_k64_s4"), \
+     pipelined<DT, T256x256_w4_k64_s4b, true>("spread256x256_w2x2_k64_s4"), \
+     pipelined<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4"),    \
+     pipelined<DT, T128x128_w4_k64_s4, true>("spread128x128_w2x2_k64_s4"), \
+     staged<DT, T256x256_w4_s2, 2>("staged256x256_w2x2_k128_n2"),          \
+     staged<DT, T256x256_w4_s2, 1>("staged256x256_w2x2_k128_n1"),          \
+     staged<DT, T256x256_w8t_s2, 1>("staged256x256_w4x2_k128_n1"),         \
+     staged<DT, T256x256_w8_s2, 1>("staged256x256_w2x4_k128_n1"),          \
+     staged<DT, T256x256_w4_k64_s2, 2>("staged256x256_w2x2_k64_n2"),       \
+     staged<DT, T256x256_w8t_k64_s2, 2>("staged256x256_w4x2_k64_n2"),      \
+     staged<DT, T128x128_w4_k128_s2, 2>("staged128x128_w2x2_k128_n2")}
 
 const Variant kF16[] = VARIANT_LIST(F16);
 const Variant kS8[] = VARIANT_LIST(S8);

@@ -130,6 +130,461 @@ __device__ __forceinline__ void compute_stage(const uint8_t *st, int wm, int wn,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Software-pipelined variant. Same tiles, LDS layout and DMA as tiled_gemm, but
+//  * operand runs are double-buffered in registers: the ds_reads of K-chunk
+//    kc+1 are issued between the MFMAs of chunk kc (sched_group_barrier
+//    interleaves one read per MFMA), so LDS latency hides under the MFMAs;
+//  * the per-slice wait + barrier sits inside the last K-chunk: half of its
+//    MFMAs run, then the barrier, then the next slice's DMA is issued and its
+//    first runs are read while the other half of the MFMAs run;
+//  * all STAGES buffers are filled up front, so each slice's copy has
+//    STAGES - 1 slices of compute to land.
+// Needs an even number of 32-byte K-chunks per slice (KCH), so chunk 0 of
+// every slice uses register set 0.
+
+template <class T>
+__device__ __forceinline__ void load_runs(const uint8_t *st, int kc, int wm, int wn, int r, int h,
+                                          i32x4 (&a)[T::FM], i32x4 (&b)[T::FN]) {
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+        const int q = wm * T::WTM + i * 32 + r;
+        a[i] = *reinterpret_cast<const i32x4 *>(st + q * T::BKB +
+                                                 (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+    }
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j) {
+        const int q = T::BM + wn * T::WTN + j * 32 + r;
+        b[j] = *reinterpret_cast<const i32x4 *>(st + q * T::BKB +
+                                                 (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+    }
+}
+
+// MFMAs of blocks p in [P0, P1) (p = i * FN + j) on one register set.
+template <int DT, class T, int P0, int P1>
+__device__ __forceinline__ void mma_runs(const i32x4 (&a)[T::FM], const i32x4 (&b)[T::FN],
+                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+#pragma unroll
+    for (int p = P0; p < P1; ++p) {
+        const int i = p / T::FN, j = p % T::FN;
+        if constexpr (DT == F16) {
+            acc[i][j] = mfma_f16(a[i], b[j], acc[i][j]);
+        } else if constexpr (DT == S8) {
+            acc[i][j] = mfma_i8(a[i], b[j], acc[i][j]);
+        } else {
+            acc[i][j] = mfma_i8(s4_lo_x16(a[i]), s4_lo_x16(b[j]), acc[i][j]);
+            acc[i][j] = mfma_i8(s4_hi_x16(a[i]), s4_hi_x16(b[j]), acc[i][j]);
+        }
+    }
+}
+
+// Scheduling hint: interleave NR LDS reads one-for-one with the first NR of
+// NM MFMAs, then the remaining MFMAs.
+template <int NM, int NR>
+__device__ __forceinline__ void interleave_hint() {
+#pragma unroll
+    for (int x = 0; x < NR && x < NM; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
+    if constexpr (NM > NR) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+}
+
+// Issue DMA loads j in [J0, J1) of this wave for K-slice kt into buffer `stage`.
+template <class T, int J0, int J1>
+__device__ __forceinline__ void issue_part(uint8_t *lds, const uint8_t *const *src, int wave,
+                                           int stage, int kt) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j) {
+        const int d = wave * T::DMA_PER_WAVE + j;
+        dma16(src[j] + (size_t)kt * T::BKB, lds + stage * T::STAGE_BYTES + d * 1024);
+    }
+}
+
+// Scheduling hint for one K-chunk: NR LDS reads and NV DMA loads, each placed
+// after one of the first NR + NV of the chunk's NM MFMAs, then the rest.
+template <int NM, int NR, int NV>
+__device__ __forceinline__ void chunk_hint() {
+#pragma unroll
+    for (int x = 0; x < NR; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    }
+#pragma unroll
+    for (int x = 0; x < NV; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load (DMA)
+    }
+    if constexpr (NM > NR + NV) __builtin_amdgcn_sched_group_barrier(0x008, NM - NR - NV, 0);
+}
+
+// DMA loads of one slice handed out over KCH issue slots: chunks 0..KCH-2
+// and the first half of the last chunk (before its barrier).
+template <class T, int C>
+struct DmaSlot {
+    static constexpr int J0 = T::DMA_PER_WAVE * C / T::KCH;
+    static constexpr int J1 = T::DMA_PER_WAVE * (C + 1) / T::KCH;
+};
+
+// DMA slot C of a slice (no-op when the slice has fewer chunks).
+template <class T, int C>
+__device__ __forceinline__ void issue_slot(uint8_t *lds, const uint8_t *const *src, int wave,
+                                           int stage, int kt) {
+    if constexpr (C < T::KCH)
+        issue_part<T, DmaSlot<T, C>::J0, DmaSlot<T, C>::J1>(lds, src, wave, stage, kt);
+}
+
+// One K-slice of the pipelined kernel (buffer kt % STAGES holds slice kt).
+// ISSUE: this slice also starts a copy. SPREAD selects where:
+//  * SPREAD: the copy of slice kt + S - 1 into the buffer freed at the
+//    previous slice's barrier, its DMA loads spread over the slice's chunks
+//    between the MFMAs (the wave's in-order issue never stalls on a burst of
+//    vector-memory instructions);
+//  * otherwise: the copy of slice kt + S, all DMA loads issued right after
+//    this slice's barrier, into the buffer that barrier frees.
+// Branch-free, so the reads, copies and MFMAs of a chunk share one
+// scheduling region.
+template <int DT, class T, bool ISSUE, bool SPREAD>
+__device__ __forceinline__ void pf_slice(uint8_t *lds, const uint8_t *const *src, int wave, int kt,
+                                         int wm, int wn, int r, int h, i32x4 (&ra)[2][T::FM],
+                                         i32x4 (&rb)[2][T::FN],
+                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+    constexpr int NB = T::FM * T::FN;        // MFMA blocks per wave
+    constexpr int MPB = (DT == S4) ? 2 : 1;  // MFMAs per block per K-chunk
+    constexpr int NRD = T::FM + T::FN;       // LDS reads per K-chunk
+    constexpr int S = T::STAGES;
+    constexpr bool SP = ISSUE && SPREAD;
+    const uint8_t *st = lds + (kt % S) * T::STAGE_BYTES;
+    const int sp_stage = (kt + S - 1) % S, sp_kt = kt + S - 1;
+#pragma unroll
+    for (int kc = 0; kc < T::KCH - 1; ++kc) {
+        const int cur = kc & 1;
+        __builtin_amdgcn_sched_barrier(0);
+        load_runs<T>(st, kc + 1, wm, wn, r, h, ra[cur ^ 1], rb[cur ^ 1]);
+        if constexpr (SP) {
+            // kc is a compile-time constant after unrolling
+            static_assert(T::KCH <= 4, "DMA slots are handed out for at most 4 chunks");
+            if (kc == 0) issue_slot<T, 0>(lds, src, wave, sp_stage, sp_kt);
+            if (kc == 1) issue_slot<T, 1>(lds, src, wave, sp_stage, sp_kt);
+            if (kc == 2) issue_slot<T, 2>(lds, src, wave, sp_stage, sp_kt);
+        }
+        mma_runs<DT, T, 0, NB>(ra[cur], rb[cur], acc);
+        if constexpr (SP) {
+            constexpr int nv = T::DMA_PER_WAVE / T::KCH + 1;
+            chunk_hint<NB * MPB, NRD, nv>();
+        } else {
+            chunk_hint<NB * MPB, NRD, 0>();
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // Last K-chunk: a quarter of its MFMAs (with the slice's last DMA loads),
+    // the barrier that publishes slice kt + 1 and frees this slice's buffer,
+    // then the next slice's first runs under the other MFMAs.
+    constexpr int last = (T::KCH - 1) & 1;
+    constexpr int PRE = NB / 4;
+    if constexpr (SP) issue_slot<T, T::KCH - 1>(lds, src, wave, sp_stage, sp_kt);
+    mma_runs<DT, T, 0, PRE>(ra[last], rb[last], acc);
+    if constexpr (SP) {
+        constexpr int nv = DmaSlot<T, T::KCH - 1>::J1 - DmaSlot<T, T::KCH - 1>::J0;
+        chunk_hint<PRE * MPB, 0, nv>();
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // slices issued so far: 0 .. kt + S - 1 (steady state); those after
+    // slice kt + 1 may stay in flight
+    if constexpr (ISSUE) wait_vm_barrier<(S - 2) * T::DMA_PER_WAVE>();
+    else wait_vm_barrier<0>();
+    if constexpr (ISSUE && !SPREAD) issue_stage<T>(lds, src, wave, kt % S, kt + S);
+    // for the final slice this reads a buffer nobody uses again; harmless
+    load_runs<T>(lds + ((kt + 1) % S) * T::STAGE_BYTES, 0, wm, wn, r, h, ra[0], rb[0]);
+    mma_runs<DT, T, PRE, NB>(ra[last], rb[last], acc);
+    chunk_hint<(NB - PRE) * MPB, NRD, (ISSUE && !SPREAD) ? T::DMA_PER_WAVE : 0>();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int DT, class T, bool SPREAD>
+__global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *__restrict__ A,
+                                                               const uint8_t *__restrict__ B,
+                                                               void *__restrict__ Cv, int M,
+                                                               int N, int Kb, int tiles_m,
+                                                               int tiles_n) {
+    static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
+    typedef typename Acc<DT>::type acc_t;
+    typedef typename Acc<DT>::out out_t;
+    constexpr int S = T::STAGES;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 31, h = lane >> 5;
+    const int wm = wave / T::WGN, wn = wave % T::WGN;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+
+    const uint8_t *src[T::DMA_PER_WAVE];
+#pragma unroll
+    for (int j = 0; j < T::DMA_PER_WAVE; ++j) {
+        const int d = wave * T::DMA_PER_WAVE + j;
+        const int q = d * T::ROWS_PER_DMA + lane / T::CH;
+        const int c = (lane % T::CH) ^ swz<T::CH>(q);
+        const uint8_t *rowp = (q < T::BM) ? A + (size_t)(tm * T::BM + q) * Kb
+                                          : B + (size_t)(tn * T::BN + (q - T::BM)) * Kb;
+        src[j] = rowp + c * 16;
+    }
+
+    acc_t acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) acc[i][j] = acc_t{};
+
+    const int KT = Kb / T::BKB;
+    // Fill the ring (all S buffers; S - 1 when later copies are spread over
+    // the slices), then wait for slice 0.
+    constexpr int PRE = SPREAD ? S - 1 : S;
+#pragma unroll
+    for (int s = 0; s < PRE; ++s)
+        if (s < KT) issue_stage<T>(lds, src, wave, s, s);
+    if (KT >= PRE) wait_vm_barrier<(PRE - 1) * T::DMA_PER_WAVE>();
+    else wait_vm_barrier<0>();
+
+    i32x4 ra[2][T::FM], rb[2][T::FN];
+    load_runs<T>(lds, 0, wm, wn, r, h, ra[0], rb[0]);
+
+    // Steady state: every slice issues one copy. Tail: the last PRE slices
+    // issue nothing and wait for all outstanding copies.
+    int kt = 0;
+    for (; kt + PRE < KT; ++kt)
+        pf_slice<DT, T, true, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
+    for (; kt < KT; ++kt)
+        pf_slice<DT, T, false, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
+
+    out_t *C = reinterpret_cast<out_t *>(Cv);
+    const long row0 = (long)tm * T::BM + wm * T::WTM + 4 * h;
+    const long col0 = (long)tn * T::BN + wn * T::WTN + r;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const long row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
+                const long col = col0 + j * 32;
+                if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                else C[row * N + col] = acc[i][j][v];
+            }
+}
+
+// ---------------------------------------------------------------------------
+// Register-staged variant. Same tiles, LDS layout and operand reads as the
+// pipelined kernel, but the global -> LDS copy goes through registers: each
+// lane loads its 16-byte chunks with ordinary global loads (NSETS slices in
+// flight, so a load has NSETS slices of compute to return) and later writes
+// them with ds_write_b128 to exactly the place the DMA would have filled. Two
+// LDS buffers; during slice kt the waves write slice kt + 1 (from register
+// set (kt + 1) % NSETS) into the buffer slice kt - 1 used, then refill that
+// register set with slice kt + 1 + NSETS. The writes go in the first half of
+// the slice's chunks, the refill loads in the second half, both interleaved
+// with MFMAs; one barrier per slice publishes the written buffer. Index
+// arithmetic near the end of K is clamped instead of branched (the surplus
+// loads re-read the last slice, the surplus writes land in a buffer no one
+// reads again), so every slice body is one scheduling region.
+
+template <class T, int J0, int J1>
+__device__ __forceinline__ void gload_part(i32x4 (&reg)[T::DMA_PER_WAVE], const uint8_t *const *src,
+                                           int kt) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j)
+        reg[j] = *reinterpret_cast<const i32x4 *>(src[j] + (size_t)kt * T::BKB);
+}
+
+template <class T, int J0, int J1>
+__device__ __forceinline__ void swrite_part(uint8_t *lds, const i32x4 (&reg)[T::DMA_PER_WAVE],
+                                            int wave, int lane, int stage) {
+#pragma unroll
+    for (int j = J0; j < J1; ++j) {
+        const int d = wave * T::DMA_PER_WAVE + j;
+        *reinterpret_cast<i32x4 *>(lds + stage * T::STAGE_BYTES + d * 1024 + lane * 16) = reg[j];
+    }
+}
+
+// Scheduling hint: NR LDS reads, NW LDS writes and NV global loads, each after
+// one MFMA, then the remaining MFMAs.
+template <int NM, int NR, int NW, int NV>
+__device__ __forceinline__ void chunk_hint_rs() {
+#pragma unroll
+    for (int x = 0; x < NR; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+#pragma unroll
+    for (int x = 0; x < NW; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+    }
+#pragma unroll
+    for (int x = 0; x < NV; ++x) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    }
+    if constexpr (NM > NR + NW + NV)
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - NR - NW - NV, 0);
+}
+
+// Part P of NP equal parts of this wave's DMA_PER_WAVE chunks.
+template <class T, int P, int NP>
+struct Part {
+    static constexpr int J0 = T::DMA_PER_WAVE * P / NP;
+    static constexpr int J1 = T::DMA_PER_WAVE * (P + 1) / NP;
+};
+
+// Chunk kc of a slice: its share of the register -> LDS writes (chunks in the
+// first half) or of the refill loads (chunks in the second half, the last
+// chunk excluded).
+template <class T, int KC>
+__device__ __forceinline__ void rs_chunk_copy(uint8_t *lds, i32x4 (&reg)[T::DMA_PER_WAVE],
+                                              const uint8_t *const *src, int wave, int lane,
+                                              int wstage, int lkt) {
+    constexpr int HALF = T::KCH / 2;
+    if constexpr (KC < HALF) {
+        swrite_part<T, Part<T, KC, HALF>::J0, Part<T, KC, HALF>::J1>(lds, reg, wave, lane, wstage);
+    } else if constexpr (KC < T::KCH - 1) {
+        constexpr int NPL = T::KCH - 1 - HALF;  // load slots
+        gload_part<T, Part<T, KC - HALF, NPL>::J0, Part<T, KC - HALF, NPL>::J1>(reg, src, lkt);
+    }
+}
+
+template <int DT, class T, int SET, int NSETS>
+__device__ __forceinline__ void rs_slice(uint8_t *lds, const uint8_t *const *src, int wave, int lane,
+                                         int kt, int KT, int wm, int wn, int r, int h,
+                                         i32x4 (&stg)[NSETS][T::DMA_PER_WAVE], i32x4 (&ra)[2][T::FM],
+                                         i32x4 (&rb)[2][T::FN],
+                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+    static_assert(T::STAGES == 2, "two LDS buffers");
+    constexpr int NB = T::FM * T::FN;
+    constexpr int MPB = (DT == S4) ? 2 : 1;
+    constexpr int NRD = T::FM + T::FN;
+    constexpr int HALF = T::KCH / 2;
+    constexpr int NPL = T::KCH - 1 - HALF;
+    const uint8_t *st = lds + (kt & 1) * T::STAGE_BYTES;
+    const int wstage = (kt + 1) & 1;
+    const int lkt = min(kt + 1 + NSETS, KT - 1);
+    // chunk bodies 0 .. KCH-2, each with compile-time chunk index
+#define MPG_RS_CHUNK(KC)                                                                       \
+    if constexpr ((KC) < T::KCH - 1) {                                                         \
+        constexpr int cur = (KC) & 1;                                                          \
+        __builtin_amdgcn_sched_barrier(0);                                                     \
+        load_runs<T>(st, (KC) + 1, wm, wn, r, h, ra[cur ^ 1], rb[cur ^ 1]);                   \
+        rs_chunk_copy<T, (KC)>(lds, stg[SET], src, wave, lane, wstage, lkt);                    \
+        mma_runs<DT, T, 0, NB>(ra[cur], rb[cur], acc);                                         \
+        if constexpr ((KC) < HALF)                                                             \
+            chunk_hint_rs<NB * MPB, NRD, Part<T, (KC), HALF>::J1 - Part<T, (KC), HALF>::J0, 0>(); \
+        else                                                                                   \
+            chunk_hint_rs<NB * MPB, NRD, 0,                                                    \
+                          Part<T, (KC) - HALF, (NPL > 0 ? NPL : 1)>::J1 -                      \
+                              Part<T, (KC) - HALF, (NPL > 0 ? NPL : 1)>::J0>();                \
+        __builtin_amdgcn_sched_barrier(0);                                                     \
+    }
+    MPG_RS_CHUNK(0)
+    MPG_RS_CHUNK(1)
+    MPG_RS_CHUNK(2)
+#undef MPG_RS_CHUNK
+    static_assert(T::KCH <= 4, "at most 4 chunks per slice");
+    // With two chunks per slice there is no load slot before the last chunk:
+    // the refill loads go with the last chunk's first MFMAs.
+    constexpr int last = (T::KCH - 1) & 1;
+    constexpr int PRE = NB / 4;
+    if constexpr (NPL == 0) gload_part<T, 0, T::DMA_PER_WAVE>(stg[SET], src, lkt);
+    mma_runs<DT, T, 0, PRE>(ra[last], rb[last], acc);
+    if constexpr (NPL == 0) chunk_hint_rs<PRE * MPB, 0, 0, T::DMA_PER_WAVE>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_barrier<63>();  // LDS writes and reads done; register loads are tracked by the compiler
+    load_runs<T>(lds + wstage * T::STAGE_BYTES, 0, wm, wn, r, h, ra[0], rb[0]);
+    mma_runs<DT, T, PRE, NB>(ra[last], rb[last], acc);
+    chunk_hint_rs<(NB - PRE) * MPB, NRD, 0, 0>();
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int DT, class T, int NSETS>
+__global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *__restrict__ A,
+                                                               const uint8_t *__restrict__ B,
+                                                               void *__restrict__ Cv, int M,
+                                                               int N, int Kb, int tiles_m,
+                                                               int tiles_n) {
+    static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
+    static_assert(NSETS == 1 || NSETS == 2, "one or two register sets in flight");
+    typedef typename Acc<DT>::type acc_t;
+    typedef typename Acc<DT>::out out_t;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 31, h = lane >> 5;
+    const int wm = wave / T::WGN, wn = wave % T::WGN;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+
+    const uint8_t *src[T::DMA_PER_WAVE];
+#pragma unroll
+    for (int j = 0; j < T::DMA_PER_WAVE; ++j) {
+        const int d = wave * T::DMA_PER_WAVE + j;
+        const int q = d * T::ROWS_PER_DMA + lane / T::CH;
+        const int c = (lane % T::CH) ^ swz<T::CH>(q);
+        const uint8_t *rowp = (q < T::BM) ? A + (size_t)(tm * T::BM + q) * Kb
+                                          : B + (size_t)(tn * T::BN + (q - T::BM)) * Kb;
+        src[j] = rowp + c * 16;
+    }
+
+    acc_t acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) acc[i][j] = acc_t{};
+
+    const int KT = Kb / T::BKB;
+    // Prologue: slice 0 into LDS buffer 0; slices 1 .. NSETS into register
+    // set s % NSETS (indices clamped to the last slice).
+    i32x4 stg[NSETS][T::DMA_PER_WAVE];
+    gload_part<T, 0, T::DMA_PER_WAVE>(stg[0], src, 0);
+    swrite_part<T, 0, T::DMA_PER_WAVE>(lds, stg[0], wave, lane, 0);
+    gload_part<T, 0, T::DMA_PER_WAVE>(stg[1 % NSETS], src, min(1, KT - 1));
+    if constexpr (NSETS == 2) gload_part<T, 0, T::DMA_PER_WAVE>(stg[0], src, min(2, KT - 1));
+    wait_vm_barrier<63>();
+
+    i32x4 ra[2][T::FM], rb[2][T::FN];
+    load_runs<T>(lds, 0, wm, wn, r, h, ra[0], rb[0]);
+
+    // slice kt writes register set (kt + 1) % NSETS
+    int kt = 0;
+    if constexpr (NSETS == 1) {
+        for (; kt < KT; ++kt)
+            rs_slice<DT, T, 0, 1>(lds, src, wave, lane, kt, KT, wm, wn, r, h, stg, ra, rb, acc);
+    } else {
+        for (; kt + 1 < KT; kt += 2) {
+            rs_slice<DT, T, 1, 2>(lds, src, wave, lane, kt, KT, wm, wn, r, h, stg, ra, rb, acc);
+            rs_slice<DT, T, 0, 2>(lds, src, wave, lane, kt + 1, KT, wm, wn, r, h, stg, ra, rb, acc);
+        }
+        if (kt < KT)
+            rs_slice<DT, T, 1, 2>(lds, src, wave, lane, kt, KT, wm, wn, r, h, stg, ra, rb, acc);
+    }
+
+    out_t *C = reinterpret_cast<out_t *>(Cv);
+    const long row0 = (long)tm * T::BM + wm * T::WTM + 4 * h;
+    const long col0 = (long)tn * T::BN + wn * T::WTN + r;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const long row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
+                const long col = col0 + j * 32;
+                if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                else C[row * N + col] = acc[i][j][v];
+            }
+}
+
 template <int DT, class T>
 __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__restrict__ A,
                                                             const uint8_t *__restrict__ B,

@@ -7,6 +7,8 @@ compiled kernel variant on shapes spanning several tiles, closed forms and
 edge cases. Integer results must match bit for bit; FP16 within a normalised
 error of 1e-3.
 """
+import re
+
 import numpy as np
 import pytest
 import torch
@@ -104,8 +106,7 @@ def _variant_shapes(dtype, v):
     name = mp.variant_name(dtype, v)
     if name.startswith("generic"):
         return [(97, 65, 130), (33, 31, 66)]
-    tile = name.split("_")[0][len("tile"):]
-    bm, bn = (int(x) for x in tile.split("x"))
+    bm, bn = (int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
     kb = int(name.split("_k")[1].split("_")[0])
     elems_per_kb = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
     return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb)]
