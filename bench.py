@@ -42,7 +42,7 @@ IN_BYTES = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 METRIC = "TFLOP/s | TOP/s at N=512–8192 for FP16, INT8, INT4; % of MFMA peak per dtype"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # rows of each N = 8192 point the CPU oracle computes for the baseline sample
-CPU_SAMPLE_ROWS = {"f16": 256, "s8": 1024, "s4": 1024}
+CPU_SAMPLE_ROWS = {"f16": 1024, "s8": 8192, "s4": 8192}
 
 
 def log(msg):
@@ -83,7 +83,19 @@ def main():
     ap.add_argument("--variant", action="append", default=[],
                     help="force a kernel variant for a point: dtype:N:variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead of the sweep, run a plain device copy of this many MiB "
+                         "--steps times (reference kernel for counter calibration)")
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("GEMM_FETCH", "GEMM_WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="rocprofv3 --pmc output folders (FETCH_SIZE, WRITE_SIZE of the GEMM run; "
+                         "the same of a --copy-mib run) -> profiles/traffic.json")
+    ap.add_argument("--copy-mib-ref", type=int, default=256,
+                    help="size of the copy the calibration folders were taken on")
     args = ap.parse_args()
+
+    if args.ingest_pmc:
+        ingest_pmc(args)
+        return
 
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -104,6 +116,15 @@ def main():
     for f in args.variant:
         d, n, v = f.split(":")
         forced[(d, int(n))] = int(v)
+
+    if args.copy_mib:
+        x = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        y = torch.empty_like(x)
+        for _ in range(args.steps):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        log(f"copied {args.copy_mib} MiB x {args.steps}")
+        return
 
     points = parse_points(args.points)
     bufs = []
@@ -215,6 +236,51 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def _read_counter(folder, counter, name_filter):
+    """Per-dispatch values of one counter from a rocprofv3 --pmc CSV folder."""
+    import csv
+    import glob
+    vals = []
+    for f in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] == counter and name_filter(r["Kernel_Name"]):
+                vals.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    if not vals:
+        raise SystemExit(f"no {counter} values in {folder}")
+    return vals
+
+
+def ingest_pmc(args):
+    """Scale the GEMM's FETCH_SIZE / WRITE_SIZE (KiB per dispatch) by what the
+    same counters read for a plain copy of known size, and store the per-launch
+    HBM-side traffic of the dominant kernel with the kernel source hash."""
+    import paper_2608_10103_amd as mp
+    gf, gw, cf, cw = args.ingest_pmc
+    is_gemm = lambda n: "mpg::" in n
+    is_copy = lambda n: "copy" in n.lower()
+    copy_kib = float(args.copy_mib_ref) * 1024.0
+    rf = float(np.median([v for _, v in _read_counter(cf, "FETCH_SIZE", is_copy)])) / copy_kib
+    wf = float(np.median([v for _, v in _read_counter(cw, "WRITE_SIZE", is_copy)])) / copy_kib
+    fetch = _read_counter(gf, "FETCH_SIZE", is_gemm)
+    write = _read_counter(gw, "WRITE_SIZE", is_gemm)
+    kname = fetch[0][0]
+    f_kib = float(np.median([v for _, v in fetch]))
+    w_kib = float(np.median([v for _, v in write]))
+    pts = parse_points(args.points)
+    dt, n, _ = pts[0]
+    v = mp.select_variant(dt, n, n, n)
+    key = f"{dt}:{n}:{mp.variant_name(dt, v)}"
+    hbm = (f_kib / rf + w_kib / wf) * 1024.0
+    out = {"kernel_source_hash": kernel_source_hash(),
+           "copy_calibration": {"mib": args.copy_mib_ref, "fetch_scale": rf, "write_scale": wf},
+           "points": {key: {"kernel_name": kname, "fetch_kib_per_launch": f_kib,
+                            "write_kib_per_launch": w_kib,
+                            "hbm_bytes_per_launch": int(hbm)}}}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    print(json.dumps(out))
 
 
 def cpu_baseline(bufs, log):

@@ -169,18 +169,32 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
     return true;
 }
 
-// Preferred tiled variants, largest tile first; a candidate is taken when it
-// supports the problem and yields at least `min_tiles` workgroups.
+// Variant indices in the tables above that the selection uses.
+enum : int {
+    V_PIPE256_W2X4 = 9,      // pipe256x256_w2x4_k128_s2
+    V_SPREAD128_K128 = 20,   // spread128x128_w2x2_k128_s4
+    V_SPREAD128_K64 = 21,    // spread128x128_w2x2_k64_s4
+    V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
+    V_PIPE64 = 13,           // pipe64x64_w1x1_k128_s4
+};
+
+// Preferred tiled variants per dtype, largest tile first; a candidate is
+// taken when it supports the problem and yields at least `min_tiles`
+// workgroups (256 = one per CU). Chosen from interleaved timings of every
+// variant at N = 512 ... 8192 on MI355X.
 struct Pref { int variant; long min_tiles; };
-const Pref kPrefs[] = {{1, 256}, {5, 128}, {7, 1}};
+const Pref kPrefF16[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS4[] = {{V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const Variant *t = table(dtype);
-    for (const Pref &p : kPrefs) {
-        const Variant &v = t[p.variant];
+    const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : kPrefS4);
+    for (int i = 0; i < 4; ++i) {
+        const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
         const long tiles = (long)(M / v.bm) * (long)(N / v.bn);
-        if (tiles >= p.min_tiles) return p.variant;
+        if (tiles >= prefs[i].min_tiles) return prefs[i].variant;
     }
     return 0;
 }

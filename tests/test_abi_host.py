@@ -92,3 +92,17 @@ def test_lds_swizzle_is_conflict_free(ch):
     # and the swizzle is a permutation of the chunks of every row
     for q in range(64):
         assert sorted(c ^ _swz(ch, q) for c in range(ch)) == list(range(ch))
+
+
+def test_selection_at_sweep_sizes():
+    """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
+    want = {
+        8192: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
+        4096: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
+        2048: ("spread128x128_w2x2_k128_s4",) * 3,
+        1024: ("spread128x128_w2x2_k64_s4",) * 3,
+        512: ("spread128x128_w2x2_k64_s4",) * 3,
+    }
+    for n, names in want.items():
+        got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
+        assert got == names, (n, got)
