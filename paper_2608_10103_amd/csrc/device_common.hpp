@@ -26,12 +26,26 @@ enum Dtype : int { F16 = 0, S8 = 1, S4 = 2 };
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 
-template <int DT> struct Acc;
-template <> struct Acc<F16> { typedef f32x16 type; typedef float out; };
-template <> struct Acc<S8> { typedef i32x16 type; typedef int32_t out; };
-template <> struct Acc<S4> { typedef i32x16 type; typedef int32_t out; };
+// Accumulator of one MS x MS MFMA block (MS = 32: 16 values per lane, MS =
+// 16: 4 values per lane) and the output element type.
+template <int DT, int MS = 32> struct Acc;
+template <> struct Acc<F16, 32> { typedef f32x16 type; typedef float out; };
+template <> struct Acc<S8, 32> { typedef i32x16 type; typedef int32_t out; };
+template <> struct Acc<S4, 32> { typedef i32x16 type; typedef int32_t out; };
+template <> struct Acc<F16, 16> { typedef f32x4 type; typedef float out; };
+template <> struct Acc<S8, 16> { typedef i32x4 type; typedef int32_t out; };
+template <> struct Acc<S4, 16> { typedef i32x4 type; typedef int32_t out; };
+
+// Row within an MS x MS block of accumulator value v of a lane in lane group
+// h (= lane / MS); the column is lane % MS. 32x32: value v covers row
+// 8 (v / 4) + 4 h + v % 4; 16x16: row 4 h + v.
+template <int MS>
+__device__ __forceinline__ constexpr int acc_row(int h, int v) {
+    return MS == 32 ? 8 * (v >> 2) + 4 * h + (v & 3) : 4 * h + v;
+}
 
 // Bytes of one element in storage: FP16 2, INT8 1; INT4 is handled as bytes of
 // two nibbles, so the row pitch in bytes is K/2.
@@ -46,6 +60,18 @@ __device__ __forceinline__ f32x16 mfma_f16(i32x4 a, i32x4 b, f32x16 c) {
 
 __device__ __forceinline__ i32x16 mfma_i8(i32x4 a, i32x4 b, i32x16 c) {
     return __builtin_amdgcn_mfma_i32_32x32x32_i8(a, b, c, 0, 0, 0);
+}
+
+// 16x16 blocks: v_mfma_f32_16x16x32_f16 and v_mfma_i32_16x16x64_i8 take the
+// same 16-byte operand run per lane; lane l owns row/column l % 16 and K-group
+// l / 16 of four.
+__device__ __forceinline__ f32x4 mfma_f16(i32x4 a, i32x4 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+                                                   __builtin_bit_cast(half8, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ i32x4 mfma_i8(i32x4 a, i32x4 b, i32x4 c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
 
 // INT4 decode for the tiled kernels, four bytes (eight nibbles) per 32-bit

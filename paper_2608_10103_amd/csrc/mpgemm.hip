@@ -29,6 +29,8 @@ typedef TileCfg<128, 128, 2, 2, 64, 4, 4> T128x128_w4_k64_s4;
 typedef TileCfg<256, 256, 2, 2, 64, 2, 4> T256x256_w4_k64_s2;
 typedef TileCfg<256, 256, 4, 2, 64, 2, 4> T256x256_w8t_k64_s2;
 typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_k128_s2;
+typedef TileCfg<256, 256, 2, 4, 64, 2, 4> T256x256_w8_k64_s2;
+typedef TileCfg<128, 128, 2, 2, 128, 4, 4, 16> T128x128_w4_s4_m16;
 typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4;
 typedef TileCfg<256, 128, 2, 2, 128, 3, 4> T256x128_w4_s3;
 typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
@@ -70,6 +72,12 @@ Variant staged(const char *name) {
     return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
 }
 
+template <int DT, class T, int LEFT>
+Variant pingpong(const char *name) {
+    kernel_fn f = &tiled_gemm_pp<DT, T, LEFT>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+}
+
 template <int DT>
 Variant generic(const char *name) {
     generic_fn f = &generic_gemm<DT>;
@@ -105,7 +113,12 @@ Variant generic(const char *name) {
      staged<DT, T256x256_w8_s2, 1>("staged256x256_w2x4_k128_n1"),          \
      staged<DT, T256x256_w4_k64_s2, 2>("staged256x256_w2x2_k64_n2"),       \
      staged<DT, T256x256_w8t_k64_s2, 2>("staged256x256_w4x2_k64_n2"),      \
-     staged<DT, T128x128_w4_k128_s2, 2>("staged128x128_w2x2_k128_n2")}
+     staged<DT, T128x128_w4_k128_s2, 2>("staged128x128_w2x2_k128_n2"),     \
+     pingpong<DT, T256x256_w8_s2, 4>("pingpong256x256_k128_c4"),          \
+     pingpong<DT, T256x256_w8_s2, 2>("pingpong256x256_k128_c2"),          \
+     pingpong<DT, T256x256_w8_s2, 6>("pingpong256x256_k128_c6"),          \
+     pingpong<DT, T256x256_w8_k64_s2, 4>("pingpong256x256_k64_c4"),       \
+     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16")}
 
 const Variant kF16[] = VARIANT_LIST(F16);
 const Variant kS8[] = VARIANT_LIST(S8);
@@ -161,7 +174,8 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
     if (v.kind == GENERIC) return true;
     if (M == 0 || N == 0 || K == 0) return false;
     const long kb = row_bytes(dtype, K);
-    if (M % v.bm || N % v.bn || kb % v.bkb) return false;
+    // edge tiles are predicated in M and N; K must fill whole slices
+    if (kb % v.bkb) return false;
     if (!aligned(A, 16) || !aligned(B, 16) || !aligned(C, 4)) return false;
     // INT4 partial sums are carried scaled by 256 (see s4_lo_x16)
     if (dtype == S4 && K >= 131072) return false;
@@ -193,8 +207,10 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     for (int i = 0; i < 4; ++i) {
         const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
-        const long tiles = (long)(M / v.bm) * (long)(N / v.bn);
-        if (tiles >= prefs[i].min_tiles) return prefs[i].variant;
+        const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
+        // skip a tile that would mostly compute padding
+        if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < 4) continue;
+        if (tm * tn >= prefs[i].min_tiles) return prefs[i].variant;
     }
     return 0;
 }
@@ -210,7 +226,7 @@ hipError_t launch(int dtype, const Variant &v, int M, int N, int K, const void *
         return hipLaunchKernel(v.fn, dim3(tiles), dim3(v.threads), args, 0, stream);
     }
     int kb = (int)row_bytes(dtype, K);
-    int tiles_m = M / v.bm, tiles_n = N / v.bn;
+    int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
     void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n};
     return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
 }

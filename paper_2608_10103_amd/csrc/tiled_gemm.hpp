@@ -24,20 +24,25 @@
 //    from LDS (ds_read_b128). INT4 runs are decoded to int8 in registers.
 //  * Epilogue: accumulators straight to C (INT4: shifted right by 8, see
 //    s4_lo_x16), each store instruction writing two 128-byte row segments.
+//  * M and N need not be multiples of the tile: edge tiles clamp their
+//    copy rows (stage_src) and mask their stores. K must fill whole slices.
 #pragma once
 
 #include "device_common.hpp"
 
 namespace mpg {
 
-template <int BM_, int BN_, int WGM_, int WGN_, int BKB_, int STAGES_, int GROUP_M_>
+template <int BM_, int BN_, int WGM_, int WGN_, int BKB_, int STAGES_, int GROUP_M_, int MS_ = 32>
 struct TileCfg {
     static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, BKB = BKB_;
     static constexpr int STAGES = STAGES_, GROUP_M = GROUP_M_;
+    static constexpr int MS = MS_;                        // MFMA block: 32x32 or 16x16
+    static constexpr int G = 64 / MS;                     // lane groups along K
+    static constexpr int NV = MS * MS / 64;               // accumulator values per lane
     static constexpr int NWAVES = WGM * WGN;
     static constexpr int NTHREADS = 64 * NWAVES;
     static constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wave sub-tile
-    static constexpr int FM = WTM / 32, FN = WTN / 32;    // MFMA blocks per wave
+    static constexpr int FM = WTM / MS, FN = WTN / MS;    // MFMA blocks per wave
     static constexpr int CH = BKB / 16;                   // 16-byte chunks per LDS row
     static constexpr int ROWS = BM + BN;                  // LDS rows per stage
     static constexpr int STAGE_BYTES = ROWS * BKB;
@@ -45,14 +50,32 @@ struct TileCfg {
     static constexpr int ROWS_PER_DMA = 1024 / BKB;       // rows one wave-wide DMA fills
     static constexpr int NDMA = ROWS / ROWS_PER_DMA;      // DMAs per stage per workgroup
     static constexpr int DMA_PER_WAVE = NDMA / NWAVES;
-    static constexpr int KCH = BKB / 32;                  // 32-byte K-chunks per stage
+    static constexpr int KCH = BKB / (16 * G);            // MFMA K-steps per stage
     static_assert(BKB == 64 || BKB == 128, "LDS rows are 64 or 128 bytes");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0 && FM >= 1 && FN >= 1, "wave tile");
+    static_assert(MS == 32 || MS == 16, "MFMA block");
+    static_assert(WTM % MS == 0 && WTN % MS == 0 && FM >= 1 && FN >= 1 && KCH >= 1, "wave tile");
     static_assert(NDMA % NWAVES == 0, "DMAs split evenly over waves");
     static_assert(BM % ROWS_PER_DMA == 0, "a DMA never straddles the A and B parts");
     static_assert(STAGES >= 2 && (STAGES - 2) * DMA_PER_WAVE <= 63, "vmcnt range");
     static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
 };
+
+// Source of lane `lane` for the copy unit d (1 KiB of LDS) of a stage:
+// LDS row q = d * ROWS_PER_DMA + lane / CH takes A row tm*BM + q or B row
+// tn*BN + q - BM; slot lane % CH of that row holds logical chunk
+// slot ^ swz(q). Rows past M (or N) are clamped to the last one: the tile's
+// edge rows then compute values nobody stores, and every load stays inside
+// the operands.
+template <class T>
+__device__ __forceinline__ const uint8_t *stage_src(const uint8_t *A, const uint8_t *B, int M,
+                                                    int N, int Kb, int tm, int tn, int d,
+                                                    int lane) {
+    const int q = d * T::ROWS_PER_DMA + lane / T::CH;
+    const int c = (lane % T::CH) ^ swz<T::CH>(q);
+    const uint8_t *rowp = (q < T::BM) ? A + (size_t)min(tm * T::BM + q, M - 1) * Kb
+                                      : B + (size_t)min(tn * T::BN + (q - T::BM), N - 1) * Kb;
+    return rowp + c * 16;
+}
 
 // Wait until at most N of this wave's vector-memory operations are pending
 // and all its LDS operations are done, then barrier the workgroup. The memory
@@ -87,21 +110,21 @@ __device__ __forceinline__ void issue_stage(uint8_t *lds, const uint8_t *const *
 // All MFMAs of one LDS buffer for this wave's sub-tile.
 template <int DT, class T>
 __device__ __forceinline__ void compute_stage(const uint8_t *st, int wm, int wn, int r, int h,
-                                              typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+                                              typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
 #pragma unroll
     for (int kc = 0; kc < T::KCH; ++kc) {
         i32x4 a[T::FM], b[T::FN];
 #pragma unroll
         for (int i = 0; i < T::FM; ++i) {
-            const int q = wm * T::WTM + i * 32 + r;
+            const int q = wm * T::WTM + i * T::MS + r;
             a[i] = *reinterpret_cast<const i32x4 *>(
-                st + q * T::BKB + (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+                st + q * T::BKB + (((T::G * kc + h) ^ swz<T::CH>(q)) << 4));
         }
 #pragma unroll
         for (int j = 0; j < T::FN; ++j) {
-            const int q = T::BM + wn * T::WTN + j * 32 + r;
+            const int q = T::BM + wn * T::WTN + j * T::MS + r;
             b[j] = *reinterpret_cast<const i32x4 *>(
-                st + q * T::BKB + (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+                st + q * T::BKB + (((T::G * kc + h) ^ swz<T::CH>(q)) << 4));
         }
         if constexpr (DT == F16) {
 #pragma unroll
@@ -148,22 +171,22 @@ __device__ __forceinline__ void load_runs(const uint8_t *st, int kc, int wm, int
                                           i32x4 (&a)[T::FM], i32x4 (&b)[T::FN]) {
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
-        const int q = wm * T::WTM + i * 32 + r;
+        const int q = wm * T::WTM + i * T::MS + r;
         a[i] = *reinterpret_cast<const i32x4 *>(st + q * T::BKB +
-                                                 (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+                                                 (((T::G * kc + h) ^ swz<T::CH>(q)) << 4));
     }
 #pragma unroll
     for (int j = 0; j < T::FN; ++j) {
-        const int q = T::BM + wn * T::WTN + j * 32 + r;
+        const int q = T::BM + wn * T::WTN + j * T::MS + r;
         b[j] = *reinterpret_cast<const i32x4 *>(st + q * T::BKB +
-                                                 (((2 * kc + h) ^ swz<T::CH>(q)) << 4));
+                                                 (((T::G * kc + h) ^ swz<T::CH>(q)) << 4));
     }
 }
 
 // MFMAs of blocks p in [P0, P1) (p = i * FN + j) on one register set.
 template <int DT, class T, int P0, int P1>
 __device__ __forceinline__ void mma_runs(const i32x4 (&a)[T::FM], const i32x4 (&b)[T::FN],
-                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+                                         typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
 #pragma unroll
     for (int p = P0; p < P1; ++p) {
         const int i = p / T::FN, j = p % T::FN;
@@ -248,7 +271,7 @@ template <int DT, class T, bool ISSUE, bool SPREAD>
 __device__ __forceinline__ void pf_slice(uint8_t *lds, const uint8_t *const *src, int wave, int kt,
                                          int wm, int wn, int r, int h, i32x4 (&ra)[2][T::FM],
                                          i32x4 (&rb)[2][T::FN],
-                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+                                         typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
     constexpr int NB = T::FM * T::FN;        // MFMA blocks per wave
     constexpr int MPB = (DT == S4) ? 2 : 1;  // MFMAs per block per K-chunk
     constexpr int NRD = T::FM + T::FN;       // LDS reads per K-chunk
@@ -308,15 +331,15 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
                                                                int N, int Kb, int tiles_m,
                                                                int tiles_n) {
     static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
-    typedef typename Acc<DT>::type acc_t;
-    typedef typename Acc<DT>::out out_t;
+    typedef typename Acc<DT, T::MS>::type acc_t;
+    typedef typename Acc<DT, T::MS>::out out_t;
     constexpr int S = T::STAGES;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int r = lane & 31, h = lane >> 5;
+    const int r = lane % T::MS, h = lane / T::MS;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
@@ -325,11 +348,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
 #pragma unroll
     for (int j = 0; j < T::DMA_PER_WAVE; ++j) {
         const int d = wave * T::DMA_PER_WAVE + j;
-        const int q = d * T::ROWS_PER_DMA + lane / T::CH;
-        const int c = (lane % T::CH) ^ swz<T::CH>(q);
-        const uint8_t *rowp = (q < T::BM) ? A + (size_t)(tm * T::BM + q) * Kb
-                                          : B + (size_t)(tn * T::BN + (q - T::BM)) * Kb;
-        src[j] = rowp + c * 16;
+        src[j] = stage_src<T>(A, B, M, N, Kb, tm, tn, d, lane);
     }
 
     acc_t acc[T::FM][T::FN];
@@ -360,18 +379,20 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
         pf_slice<DT, T, false, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
 
     out_t *C = reinterpret_cast<out_t *>(Cv);
-    const long row0 = (long)tm * T::BM + wm * T::WTM + 4 * h;
+    const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
         for (int j = 0; j < T::FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const long row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
-                const long col = col0 + j * 32;
-                if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                else C[row * N + col] = acc[i][j][v];
+            for (int v = 0; v < T::NV; ++v) {
+                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
+                const long col = col0 + j * T::MS;
+                if (row < M && col < N) {
+                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                    else C[row * N + col] = acc[i][j][v];
+                }
             }
 }
 
@@ -459,7 +480,7 @@ __device__ __forceinline__ void rs_slice(uint8_t *lds, const uint8_t *const *src
                                          int kt, int KT, int wm, int wn, int r, int h,
                                          i32x4 (&stg)[NSETS][T::DMA_PER_WAVE], i32x4 (&ra)[2][T::FM],
                                          i32x4 (&rb)[2][T::FN],
-                                         typename Acc<DT>::type (&acc)[T::FM][T::FN]) {
+                                         typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
     static_assert(T::STAGES == 2, "two LDS buffers");
     constexpr int NB = T::FM * T::FN;
     constexpr int MPB = (DT == S4) ? 2 : 1;
@@ -513,14 +534,14 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *_
                                                                int tiles_n) {
     static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
     static_assert(NSETS == 1 || NSETS == 2, "one or two register sets in flight");
-    typedef typename Acc<DT>::type acc_t;
-    typedef typename Acc<DT>::out out_t;
+    typedef typename Acc<DT, T::MS>::type acc_t;
+    typedef typename Acc<DT, T::MS>::out out_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int r = lane & 31, h = lane >> 5;
+    const int r = lane % T::MS, h = lane / T::MS;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
@@ -529,11 +550,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *_
 #pragma unroll
     for (int j = 0; j < T::DMA_PER_WAVE; ++j) {
         const int d = wave * T::DMA_PER_WAVE + j;
-        const int q = d * T::ROWS_PER_DMA + lane / T::CH;
-        const int c = (lane % T::CH) ^ swz<T::CH>(q);
-        const uint8_t *rowp = (q < T::BM) ? A + (size_t)(tm * T::BM + q) * Kb
-                                          : B + (size_t)(tn * T::BN + (q - T::BM)) * Kb;
-        src[j] = rowp + c * 16;
+        src[j] = stage_src<T>(A, B, M, N, Kb, tm, tn, d, lane);
     }
 
     acc_t acc[T::FM][T::FN];
@@ -570,18 +587,215 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *_
     }
 
     out_t *C = reinterpret_cast<out_t *>(Cv);
-    const long row0 = (long)tm * T::BM + wm * T::WTM + 4 * h;
+    const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
         for (int j = 0; j < T::FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const long row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
-                const long col = col0 + j * 32;
-                if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                else C[row * N + col] = acc[i][j][v];
+            for (int v = 0; v < T::NV; ++v) {
+                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
+                const long col = col0 + j * T::MS;
+                if (row < M && col < N) {
+                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                    else C[row * N + col] = acc[i][j][v];
+                }
+            }
+}
+
+// ---------------------------------------------------------------------------
+// Ping-pong variant: 8 waves in two groups of 4, group g computing rows
+// [128 g, 128 g + 128) of a 256 x 256 tile (wave tiles 128 x 64), the groups
+// offset by one phase. Each K-slice takes two phases separated by workgroup
+// barriers; in every phase one group runs the slice's MFMAs from LDS while
+// the other writes its share of later slices from registers to LDS and
+// issues its next global loads, so the MFMA pipe of each SIMD is fed by one
+// wave while the other does the memory work, and a barrier never drains it:
+// each group issues the last LEFT MFMA blocks of a slice after the barrier
+// that ends its compute phase, while the other group's first LDS reads are in
+// flight.
+//
+// Copy duties (two LDS buffers, buffer k % 2 holds slice k):
+//   group 0, phase 2k+1: A rows 0..127 and B rows 0..127 of slice k+1;
+//   group 1, phase 2k:   A rows 128..255 of slice k and B rows 128..255 of
+//                        slice k+1.
+// Group 0 computes slice k in phase 2k, group 1 in phase 2k+1. Every write
+// lands in a buffer region whose last reader finished at least one barrier
+// earlier, and every slice is complete one barrier before its first reader.
+// Register loads run one copy phase (two phases) ahead of their writes.
+
+template <class T>
+struct PingPong {
+    static constexpr int NA = T::BM * T::BKB / 1024;  // 1 KiB units of the A part
+    static constexpr int NB = T::BN * T::BKB / 1024;  // units of the B part
+    static constexpr int UA = NA / 8, UB = NB / 8;    // per wave
+    static constexpr int U = UA + UB;
+    static_assert(T::BM == 256 && T::BN == 256 && T::WGM == 2 && T::WGN == 4 && T::STAGES == 2,
+                  "ping-pong needs 256 x 256 tiles, 2 x 4 waves, two buffers");
+    static_assert(NA % 8 == 0 && NB % 8 == 0, "units split over the waves");
+};
+
+// Unit index (LDS 1 KiB block of a stage) of this wave's copy slot j.
+template <class T>
+__device__ __forceinline__ int pp_unit(int g, int w4, int j) {
+    typedef PingPong<T> P;
+    return (j < P::UA) ? g * (P::NA / 2) + w4 * P::UA + j
+                       : P::NA + g * (P::NB / 2) + w4 * P::UB + (j - P::UA);
+}
+
+template <int DT, class T, int LEFT>
+__device__ __forceinline__ void pp_compute(const uint8_t *st, int wm, int wn, int r, int h,
+                                           i32x4 (&ra)[2][T::FM], i32x4 (&rb)[2][T::FN],
+                                           typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
+    constexpr int NBK = T::FM * T::FN;
+    constexpr int MPB = (DT == S4) ? 2 : 1;
+    constexpr int NRD = T::FM + T::FN;
+    constexpr int last = (T::KCH - 1) & 1;
+    __builtin_amdgcn_sched_barrier(0);
+    load_runs<T>(st, 0, wm, wn, r, h, ra[0], rb[0]);
+#pragma unroll
+    for (int kc = 0; kc < T::KCH - 1; ++kc) {
+        const int cur = kc & 1;
+        __builtin_amdgcn_sched_barrier(0);
+        load_runs<T>(st, kc + 1, wm, wn, r, h, ra[cur ^ 1], rb[cur ^ 1]);
+        mma_runs<DT, T, 0, NBK>(ra[cur], rb[cur], acc);
+        chunk_hint<NBK * MPB, NRD, 0>();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    mma_runs<DT, T, 0, NBK - LEFT>(ra[last], rb[last], acc);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_barrier<63>();
+}
+
+// Copy phase: the LEFT MFMA blocks the group carried over (if any), the
+// register -> LDS writes of this wave's slots, then the refill loads.
+// Slots j < UA go to buffer `sa` (A part), the others to buffer `sb`.
+template <int DT, class T, int LEFT, bool CARRY>
+__device__ __forceinline__ void pp_copy(uint8_t *lds, const uint8_t *const *src,
+                                        i32x4 (&stg)[PingPong<T>::U], int g, int w4, int lane,
+                                        int sa, int sb, int lka, int lkb, i32x4 (&ra)[2][T::FM],
+                                        i32x4 (&rb)[2][T::FN],
+                                        typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
+    typedef PingPong<T> P;
+    constexpr int NBK = T::FM * T::FN;
+    constexpr int MPB = (DT == S4) ? 2 : 1;
+    constexpr int last = (T::KCH - 1) & 1;
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (CARRY) mma_runs<DT, T, NBK - LEFT, NBK>(ra[last], rb[last], acc);
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) {
+        const int d = pp_unit<T>(g, w4, j);
+        const int stage = (j < P::UA) ? sa : sb;
+        *reinterpret_cast<i32x4 *>(lds + stage * T::STAGE_BYTES + d * 1024 + lane * 16) = stg[j];
+    }
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) {
+        const int kt = (j < P::UA) ? lka : lkb;
+        stg[j] = *reinterpret_cast<const i32x4 *>(src[j] + (size_t)kt * T::BKB);
+    }
+    if constexpr (CARRY) chunk_hint_rs<LEFT * MPB, 0, P::U, P::U>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm_barrier<63>();
+}
+
+template <int DT, class T, int LEFT>
+__global__ __launch_bounds__(512, 1) void tiled_gemm_pp(const uint8_t *__restrict__ A,
+                                                       const uint8_t *__restrict__ B,
+                                                       void *__restrict__ Cv, int M, int N, int Kb,
+                                                       int tiles_m, int tiles_n) {
+    typedef PingPong<T> P;
+    static_assert(T::NTHREADS == 512, "8 waves");
+    static_assert(LEFT >= 1 && LEFT < T::FM * T::FN, "carried MFMA blocks");
+    typedef typename Acc<DT, T::MS>::type acc_t;
+    typedef typename Acc<DT, T::MS>::out out_t;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane % T::MS, h = lane / T::MS;
+    const int g = wave / T::WGN, w4 = wave % T::WGN;  // group = wave row
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+
+    const uint8_t *src[P::U];
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) {
+        const int d = pp_unit<T>(g, w4, j);
+        src[j] = stage_src<T>(A, B, M, N, Kb, tm, tn, d, lane);
+    }
+
+    acc_t acc[T::FM][T::FN];
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j) acc[i][j] = acc_t{};
+
+    const int KT = Kb / T::BKB;
+    i32x4 stg[P::U];
+    i32x4 ra[2][T::FM], rb[2][T::FN];
+    // Prologue: group 0 writes its A and B parts of slice 0 and loads slice 1;
+    // group 1 writes its B part of slice 0 and loads its A part of slice 0 and
+    // its B part of slice 1 (indices clamped to the last slice).
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) stg[j] = *reinterpret_cast<const i32x4 *>(src[j]);
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) {
+        if (g == 1 && j < P::UA) continue;
+        const int d = pp_unit<T>(g, w4, j);
+        *reinterpret_cast<i32x4 *>(lds + d * 1024 + lane * 16) = stg[j];
+    }
+    const int k1 = min(1, KT - 1);
+#pragma unroll
+    for (int j = 0; j < P::U; ++j) {
+        const int kt = (g == 1 && j < P::UA) ? 0 : k1;
+        stg[j] = *reinterpret_cast<const i32x4 *>(src[j] + (size_t)kt * T::BKB);
+    }
+    wait_vm_barrier<63>();
+
+    // Phase sequence (one barrier per phase):
+    //   group 0: C(0) M(0) C(1) M(1) ... C(KT-1) [carry]
+    //   group 1: M'(0) C(0) M'(1) C(1) ... M'(KT-1) C(KT-1) [carry]
+    // with C(k) = MFMAs of slice k from buffer k % 2, M(k) = write A0, B0 of
+    // slice k+1 and load slice k+2, M'(k) = write A1 of slice k and B1 of
+    // slice k+1, load A1 of slice k+1 and B1 of slice k+2. Both groups run
+    // the same loop body "C(k), copy"; group 1 enters it one phase later.
+    if (g == 1)
+        pp_copy<DT, T, LEFT, false>(lds, src, stg, g, w4, lane, 0, min(1, KT - 1) & 1,
+                                    min(1, KT - 1), min(2, KT - 1), ra, rb, acc);
+    for (int k = 0; k + 1 < KT; ++k) {
+        pp_compute<DT, T, LEFT>(lds + (k & 1) * T::STAGE_BYTES, g, w4, r, h, ra, rb, acc);
+        // group 0: M(k); group 1: M'(k + 1)
+        const int sa = (k + 1) & 1;
+        const int sb = (g == 0) ? (k + 1) & 1 : k & 1;
+        const int lka = min(k + 2, KT - 1);
+        const int lkb = min(g == 0 ? k + 2 : k + 3, KT - 1);
+        pp_copy<DT, T, LEFT, true>(lds, src, stg, g, w4, lane, sa, sb, lka, lkb, ra, rb, acc);
+    }
+    pp_compute<DT, T, LEFT>(lds + ((KT - 1) & 1) * T::STAGE_BYTES, g, w4, r, h, ra, rb, acc);
+    {
+        constexpr int last = (T::KCH - 1) & 1;
+        mma_runs<DT, T, T::FM * T::FN - LEFT, T::FM * T::FN>(ra[last], rb[last], acc);
+    }
+    // group 0's last phase, matching the barrier of group 1's last compute
+    if (g == 0) wait_vm_barrier<63>();
+
+    out_t *C = reinterpret_cast<out_t *>(Cv);
+    const long row0 = (long)tm * T::BM + g * T::WTM;
+    const long col0 = (long)tn * T::BN + w4 * T::WTN + r;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < T::NV; ++v) {
+                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
+                const long col = col0 + j * T::MS;
+                if (row < M && col < N) {
+                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                    else C[row * N + col] = acc[i][j][v];
+                }
             }
 }
 
@@ -590,14 +804,14 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__re
                                                             const uint8_t *__restrict__ B,
                                                             void *__restrict__ Cv, int M, int N,
                                                             int Kb, int tiles_m, int tiles_n) {
-    typedef typename Acc<DT>::type acc_t;
-    typedef typename Acc<DT>::out out_t;
+    typedef typename Acc<DT, T::MS>::type acc_t;
+    typedef typename Acc<DT, T::MS>::out out_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int r = lane & 31, h = lane >> 5;
+    const int r = lane % T::MS, h = lane / T::MS;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
@@ -607,11 +821,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__re
 #pragma unroll
     for (int j = 0; j < T::DMA_PER_WAVE; ++j) {
         const int d = wave * T::DMA_PER_WAVE + j;
-        const int q = d * T::ROWS_PER_DMA + lane / T::CH;  // LDS row
-        const int c = (lane % T::CH) ^ swz<T::CH>(q);       // logical chunk for this slot
-        const uint8_t *rowp = (q < T::BM) ? A + (size_t)(tm * T::BM + q) * Kb
-                                          : B + (size_t)(tn * T::BN + (q - T::BM)) * Kb;
-        src[j] = rowp + c * 16;
+        src[j] = stage_src<T>(A, B, M, N, Kb, tm, tn, d, lane);
     }
 
     acc_t acc[T::FM][T::FN];
@@ -634,18 +844,20 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__re
     }
 
     out_t *C = reinterpret_cast<out_t *>(Cv);
-    const long row0 = (long)tm * T::BM + wm * T::WTM + 4 * h;
+    const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
         for (int j = 0; j < T::FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const long row = row0 + i * 32 + 8 * (v >> 2) + (v & 3);
-                const long col = col0 + j * 32;
-                if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                else C[row * N + col] = acc[i][j][v];
+            for (int v = 0; v < T::NV; ++v) {
+                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
+                const long col = col0 + j * T::MS;
+                if (row < M && col < N) {
+                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
+                    else C[row * N + col] = acc[i][j][v];
+                }
             }
 }
 

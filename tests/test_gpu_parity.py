@@ -109,7 +109,9 @@ def _variant_shapes(dtype, v):
     bm, bn = (int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
     kb = int(name.split("_k")[1].split("_")[0])
     elems_per_kb = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
-    return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb)]
+    return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb),
+            # ragged M and N: predicated edge tiles
+            (2 * bm + 17, bn + 5, 3 * elems_per_kb), (1, bn - 1, elems_per_kb), (bm + 31, 1, 2 * elems_per_kb)]
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
@@ -216,11 +218,18 @@ def test_edge_shapes(dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_ragged_large(dtype):
-    """Sizes just off the tile grid go to the bounds-checked kernel."""
+    """K off the slice grid goes to the bounds-checked kernel; ragged M and N
+    with whole slices stay on the tiled kernels with predicated edges."""
     M, N, K = 1000, 777, 1030
     A, B = si.gen_operands(dtype, M, N, K, seed=4242)
     assert mp.select_variant(dtype, M, N, K) == 0
     assert_parity(dtype, gpu_gemm(dtype, A, B), *oracle_gemm(dtype, A, B), f"{dtype} ragged")
+    for (M, N, K) in [(1000, 777, 1024), (4097, 300, 512), (16, 4096, 1024), (3000, 5, 256)]:
+        A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
+        v = mp.select_variant(dtype, M, N, K)
+        assert v > 0, (M, N, K)
+        assert_parity(dtype, gpu_gemm(dtype, A, B), *oracle_gemm(dtype, A, B),
+                      f"{dtype} {M}x{N}x{K} {mp.variant_name(dtype, v)}")
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
