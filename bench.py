@@ -34,9 +34,16 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-# Published dense (non-sparse) MFMA peaks of the MI355X, in T(FL)OP/s. INT4 runs
-# on the INT8 MFMA (gfx950 has no 4-bit integer MFMA), so its peak is INT8's.
+# Published dense (non-sparse) MFMA peaks of the MI355X, in T(FL)OP/s. gfx950
+# has no 4-bit integer MFMA: INT4 runs either on the INT8 MFMA (peak 5000) or,
+# converted to FP6, on the FP6 MFMA (peak 10100); a point is priced at the
+# peak of the MFMA its kernel uses.
 PEAK = {"f16": 2500.0, "s8": 5000.0, "s4": 5000.0}
+PEAK_FP6 = 10100.0
+
+
+def point_peak(dtype: str, variant_name: str) -> float:
+    return PEAK_FP6 if variant_name.startswith("fp6") else PEAK[dtype]
 PEAK_UNIT = {"f16": "TFLOP/s", "s8": "TOP/s", "s4": "TOP/s"}
 IN_BYTES = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 METRIC = "TFLOP/s | TOP/s at N=512–8192 for FP16, INT8, INT4; % of MFMA peak per dtype"
@@ -182,7 +189,7 @@ def main():
         tops = ops / (mean_ms * 1e-3) / 1e12
         pts.append(dict(dtype=b["dt"], n=b["n"], variant=b["vname"], ms=round(mean_ms, 5),
                         ms_min=round(float(np.min(ms)), 5), ms_max=round(float(np.max(ms)), 5),
-                        tops=round(tops, 2), frac_peak=round(tops / PEAK[b["dt"]], 4),
+                        tops=round(tops, 2), frac_peak=round(tops / point_peak(b["dt"], b["vname"]), 4),
                         total_ms=mean_ms * args.steps))
 
     dom = max(pts, key=lambda p: p["total_ms"])
@@ -198,8 +205,9 @@ def main():
         except (ValueError, KeyError, OSError):
             traffic = None
     roofline = dict(bound="mfma", kernel=f'{dom["dtype"]} N={n} {dom["variant"]}',
-                    achieved=round(dom["tops"], 2), peak=PEAK[dom["dtype"]],
-                    unit=PEAK_UNIT[dom["dtype"]], frac=round(dom["tops"] / PEAK[dom["dtype"]], 4),
+                    achieved=round(dom["tops"], 2), peak=point_peak(dom["dtype"], dom["variant"]),
+                    unit=PEAK_UNIT[dom["dtype"]],
+                    frac=round(dom["tops"] / point_peak(dom["dtype"], dom["variant"]), 4),
                     traffic=traffic,
                     algorithmic_bytes=int((2 * IN_BYTES[dom["dtype"]] + 4) * n * n),
                     algorithmic_ops=int(2 * n ** 3))

@@ -21,21 +21,34 @@
  * Memory and ownership. A, B and C are DEVICE pointers on the current HIP
  * device, owned by the caller; the library never allocates, frees or copies
  * them and keeps no pointer after the call returns. C must not overlap A or B.
- * Any alignment is accepted; 16-byte aligned operands whose shapes match a
- * tuned tile take the fast kernels, everything else a bounds-checked kernel.
+ * Any alignment is accepted; operands whose shapes and alignment suit a tuned
+ * tile take the fast kernels, everything else a bounds-checked kernel.
+ * Workspace: the INT4 kernels on the FP6 matrix cores first convert A and B
+ * into a device workspace of 24 * (ceil(M/256) + ceil(N/256)) * 256 *
+ * ceil(K/256) * 8 bytes (0.75 byte per padded element). The library keeps
+ * one such buffer per (device, stream) pair (hipStreamPerThread: per host
+ * thread): allocated with hipMalloc on the stream's first such call, grown
+ * when a larger problem arrives (that call first synchronises the stream,
+ * whose earlier calls may still read the old buffer), and held until the
+ * process ends. Calls on one stream reuse it in stream order; calls on
+ * different streams never share one. A stream handle that is destroyed while
+ * INT4 work is still pending on it must not be reused by a new stream for
+ * INT4 calls before that work has finished.
  *
- * Streams. Work is enqueued on `stream` (0 = the null stream) and the call
- * returns without synchronising. Calls on different streams may run
- * concurrently; the library holds no mutable state shared between calls.
- * Faults inside a kernel surface at the caller's next synchronisation of the
- * stream, not in the return value.
+ * Streams. Work is enqueued on `stream` (0 = the null stream), which must
+ * belong to the current device, and the call returns without synchronising.
+ * Calls on different streams may run concurrently. Faults inside a kernel
+ * surface at the caller's next synchronisation of the stream, not in the
+ * return value.
  *
  * Errors. Each entry point returns hipSuccess or:
  *   hipErrorInvalidValue  M, N or K negative; K odd for INT4; a required
  *                         pointer NULL (A and B when M, N, K > 0; C when
  *                         M, N > 0); C overlapping A or B; a problem whose
  *                         element counts overflow 64-bit byte offsets;
- *   the launch error      if the kernel launch itself fails.
+ *   hipErrorOutOfMemory   (INT4) the workspace could not be allocated, or
+ *                         the error of synchronising the stream to grow it;
+ *   the launch error      if a kernel launch itself fails.
  * Nothing is enqueued when an argument error is returned.
  * Degenerate sizes: M == 0 or N == 0 is a no-op returning hipSuccess; K == 0
  * writes zeros to C (empty sums).
@@ -71,7 +84,10 @@ hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, in
  * two's-complement nibbles packed two per byte along K, the low nibble holding
  * the even k: A is M rows of K/2 bytes, B is N rows of K/2 bytes. Exact
  * whenever every partial sum fits in int32, which always holds for K < 2^25
- * (|a*b| <= 64). */
+ * (|a*b| <= 64). gfx950 has no 4-bit integer MFMA: for K <= 2^18 the values
+ * are converted to FP6 E3M2 (which represents -8..8 exactly) and multiplied
+ * on the FP6 MFMA, whose FP32 accumulation is exact below 2^24; other
+ * problems run on the INT8 MFMA or the bounds-checked kernel. */
 hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
                        hipStream_t stream);
 
@@ -101,6 +117,15 @@ int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const v
  * support the arguments. C is float* for dtype 0, int32_t* otherwise. */
 hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const void *A,
                               const void *B, void *C, hipStream_t stream);
+
+/* Host-side view of the INT4 -> FP6 conversion the FP6 kernels apply on the
+ * device (same source): `in` is one run of 16 HOST bytes = 32 nibbles, word
+ * d = bytes 4d..4d+3 (little-endian); `out` (6 words, HOST) receives a
+ * 192-bit little-endian string of 32 six-bit E3M2 codes, field f at bits
+ * [6f, 6f+6). Field 8d + 4h + i holds the code of the nibble in byte i of
+ * word d, low nibble for h = 0, high nibble for h = 1 (i.e. k offset
+ * 8d + 2i + h). For tests of the encoding; never touches the GPU. */
+void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out);
 
 #ifdef __cplusplus
 }

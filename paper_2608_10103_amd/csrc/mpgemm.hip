@@ -1,17 +1,25 @@
 // mpgemm.hip - the C-ABI entry points: argument checks, kernel choice, launch.
 //
 // Every entry point validates its arguments on the host, picks a kernel
-// variant (a tiled kernel when the problem is tile-aligned and 16-byte
-// aligned, the bounds-checked kernel otherwise) and launches it on the
-// caller's stream with hipLaunchKernel, returning the launch status. Nothing
-// here allocates, copies or synchronises.
+// variant (a tiled kernel when the problem fits its constraints, the
+// bounds-checked kernel otherwise) and launches it on the caller's stream with
+// hipLaunchKernel, returning the launch status. Nothing here copies or
+// synchronises, except that the INT4 variants on the FP6 matrix cores keep a
+// workspace for the converted operands per (device, stream), allocated on
+// first use and grown (after synchronising that stream) when a larger problem
+// arrives.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <thread>
+#include <vector>
+
 #include "mpgemm.h"
 #include "generic_gemm.hpp"
 #include "tiled_gemm.hpp"
+#include "f6_gemm.hpp"
 
 using namespace mpg;
 
@@ -37,16 +45,26 @@ typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
 typedef TileCfg<128, 128, 2, 2, 128, 4, 4> T128x128_w4_s4;
 typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
 
+//             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
+typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
+typedef F6Cfg<256, 256, 2, 4, 4, 2, 4> F6_256x256_w8_s2;
+typedef F6Cfg<256, 256, 2, 2, 4, 3, 4> F6_256x256_w4_s3;
+typedef F6Cfg<256, 256, 4, 2, 4, 3, 4> F6_256x256_w8t_s3;
+typedef F6Cfg<256, 128, 2, 2, 4, 4, 4> F6_256x128_w4_s4;
+typedef F6Cfg<128, 128, 2, 2, 4, 4, 4> F6_128x128_w4_s4;
+typedef F6Cfg<128, 128, 2, 2, 4, 6, 4> F6_128x128_w4_s6;
+typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
+
 }  // namespace mpg
 
 namespace {
 
-enum Kind { GENERIC = 0, TILED = 1 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2 };
 
 struct Variant {
     const char *name;
     int kind;
-    int bm, bn, bkb;  // tile (TILED only)
+    int bm, bn, bkb;  // tile; bkb: bytes per row per K-slice (TILED), runs per stage (FP6)
     int threads;
     const void *fn;
 };
@@ -78,6 +96,14 @@ Variant pingpong(const char *name) {
     return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
 }
 
+template <class T>
+Variant fp6(const char *name) {
+    typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
+                          int32_t *, int, int, int, int, int, int, int);
+    f6_fn f = &f6_gemm<T>;
+    return Variant{name, FP6, T::BM, T::BN, T::J, T::NTHREADS, reinterpret_cast<const void *>(f)};
+}
+
 template <int DT>
 Variant generic(const char *name) {
     generic_fn f = &generic_gemm<DT>;
@@ -85,7 +111,7 @@ Variant generic(const char *name) {
 }
 
 #define VARIANT_LIST(DT)                                                   \
-    {generic<DT>("generic_32x32"),                                         \
+    generic<DT>("generic_32x32"),                                          \
      tiled<DT, T256x256_w4_s2>("tile256x256_w2x2_k128_s2"),                \
      tiled<DT, T256x256_w8_s2>("tile256x256_w2x4_k128_s2"),                \
      tiled<DT, T256x256_w4_k64_s4>("tile256x256_w2x2_k64_s4"),             \
@@ -118,14 +144,23 @@ Variant generic(const char *name) {
      pingpong<DT, T256x256_w8_s2, 2>("pingpong256x256_k128_c2"),          \
      pingpong<DT, T256x256_w8_s2, 6>("pingpong256x256_k128_c6"),          \
      pingpong<DT, T256x256_w8_k64_s2, 4>("pingpong256x256_k64_c4"),       \
-     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16")}
+     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16")
 
-const Variant kF16[] = VARIANT_LIST(F16);
-const Variant kS8[] = VARIANT_LIST(S8);
-const Variant kS4[] = VARIANT_LIST(S4);
-constexpr int kNumVariants = sizeof(kF16) / sizeof(kF16[0]);
-static_assert(sizeof(kS8) / sizeof(kS8[0]) == kNumVariants, "");
-static_assert(sizeof(kS4) / sizeof(kS4[0]) == kNumVariants, "");
+const Variant kF16[] = {VARIANT_LIST(F16)};
+const Variant kS8[] = {VARIANT_LIST(S8)};
+// INT4 also runs on the FP6 matrix cores (f6_gemm.hpp); "k" is k per stage.
+const Variant kS4[] = {VARIANT_LIST(S4),
+                       fp6<F6_256x256_w8_s3>("fp6pipe256x256_w2x4_k128_s3"),
+                       fp6<F6_256x256_w8_s2>("fp6pipe256x256_w2x4_k128_s2"),
+                       fp6<F6_256x256_w4_s3>("fp6pipe256x256_w2x2_k128_s3"),
+                       fp6<F6_256x256_w8t_s3>("fp6pipe256x256_w4x2_k128_s3"),
+                       fp6<F6_256x128_w4_s4>("fp6pipe256x128_w2x2_k128_s4"),
+                       fp6<F6_128x128_w4_s4>("fp6pipe128x128_w2x2_k128_s4"),
+                       fp6<F6_128x128_w4_s6>("fp6pipe128x128_w2x2_k128_s6"),
+                       fp6<F6_128x128_w4_k256_s3>("fp6pipe128x128_w2x2_k256_s3")};
+constexpr int kNumF16 = sizeof(kF16) / sizeof(kF16[0]);
+constexpr int kNumS8 = sizeof(kS8) / sizeof(kS8[0]);
+constexpr int kNumS4 = sizeof(kS4) / sizeof(kS4[0]);
 
 const Variant *table(int dtype) {
     switch (dtype) {
@@ -133,6 +168,15 @@ const Variant *table(int dtype) {
         case S8: return kS8;
         case S4: return kS4;
         default: return nullptr;
+    }
+}
+
+int num_variants(int dtype) {
+    switch (dtype) {
+        case F16: return kNumF16;
+        case S8: return kNumS8;
+        case S4: return kNumS4;
+        default: return -1;
     }
 }
 
@@ -169,10 +213,21 @@ bool valid_args(int dtype, int M, int N, int K, const void *A, const void *B, co
     return true;
 }
 
+// FP6 path limits: partial sums stay exact in FP32 while K <= 2^18 (after
+// padding); the conversion grid indexes rows in 32-row blocks (grid.y).
+constexpr long kF6MaxK = 1L << 18;
+constexpr long kF6MaxRows = 65535L * 32;
+
 bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, const void *B,
               const void *C) {
     if (v.kind == GENERIC) return true;
     if (M == 0 || N == 0 || K == 0) return false;
+    if (v.kind == FP6) {
+        if (dtype != S4) return false;
+        if (F6Geom::runs_pad(K) * 32 > kF6MaxK) return false;
+        if (F6Geom::rows_pad(M) > kF6MaxRows || F6Geom::rows_pad(N) > kF6MaxRows) return false;
+        return aligned(C, 4);
+    }
     const long kb = row_bytes(dtype, K);
     // edge tiles are predicated in M and N; K must fill whole slices
     if (kb % v.bkb) return false;
@@ -190,6 +245,7 @@ enum : int {
     V_SPREAD128_K64 = 21,    // spread128x128_w2x2_k64_s4
     V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
     V_PIPE64 = 13,           // pipe64x64_w1x1_k128_s4
+    V_FP6_256_S2 = 35,       // fp6pipe256x256_w2x4_k128_s2 (INT4 only)
 };
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
@@ -197,28 +253,119 @@ enum : int {
 // workgroups (256 = one per CU). Chosen from interleaved timings of every
 // variant at N = 512 ... 8192 on MI355X.
 struct Pref { int variant; long min_tiles; };
+// INT4: the FP6 kernel once the grid has at least two 256x256 tiles per CU
+// (below that its operand conversion does not pay off), then the INT8-MFMA
+// kernels.
 const Pref kPrefF16[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
+                        {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const Variant *t = table(dtype);
     const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : kPrefS4);
-    for (int i = 0; i < 4; ++i) {
+    const int n = dtype == F16 ? (int)(sizeof(kPrefF16) / sizeof(Pref))
+                               : (dtype == S8 ? (int)(sizeof(kPrefS8) / sizeof(Pref))
+                                              : (int)(sizeof(kPrefS4) / sizeof(Pref)));
+    for (int i = 0; i < n; ++i) {
         const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
         const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
         // skip a tile that would mostly compute padding
-        if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < 4) continue;
+        if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < n) continue;
         if (tm * tn >= prefs[i].min_tiles) return prefs[i].variant;
     }
     return 0;
+}
+
+// FP6 workspaces: one device buffer per (device, stream) pair, so calls on
+// one stream reuse it in stream order and calls on different streams never
+// share one. A buffer grows when a larger problem arrives: the stream is
+// synchronised first (earlier calls on it may still read the old buffer),
+// then the old buffer is freed and a larger one allocated. Buffers are kept
+// until the process ends. hipStreamPerThread names a different stream in
+// every host thread, so it is keyed by thread as well.
+struct Workspace {
+    int dev;
+    hipStream_t stream;
+    std::thread::id thread;
+    void *ptr;
+    size_t bytes;
+};
+
+hipError_t stream_workspace(hipStream_t stream, size_t bytes, void **out) {
+    static std::mutex mu;
+    static std::vector<Workspace> spaces;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const std::thread::id tid =
+        stream == hipStreamPerThread ? std::this_thread::get_id() : std::thread::id();
+    std::lock_guard<std::mutex> lock(mu);
+    Workspace *w = nullptr;
+    for (Workspace &s : spaces)
+        if (s.dev == dev && s.stream == stream && s.thread == tid) w = &s;
+    if (w && w->bytes >= bytes) {
+        *out = w->ptr;
+        return hipSuccess;
+    }
+    if (w) {
+        e = hipStreamSynchronize(stream);
+        if (e != hipSuccess) return e;
+        e = hipFree(w->ptr);
+        w->ptr = nullptr;
+        w->bytes = 0;
+        if (e != hipSuccess) return e;
+    }
+    const size_t granule = (size_t)2 << 20;
+    const size_t want = (bytes + granule - 1) / granule * granule;
+    void *p = nullptr;
+    e = hipMalloc(&p, want);
+    if (e != hipSuccess) return e;
+    if (!w) {
+        spaces.push_back(Workspace{dev, stream, tid, nullptr, 0});
+        w = &spaces.back();
+    }
+    w->ptr = p;
+    w->bytes = want;
+    *out = p;
+    return hipSuccess;
+}
+
+// INT4 on the FP6 matrix cores: convert both operands into the stream's
+// workspace, then run the FP6 tile kernel.
+hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, const uint8_t *B,
+                      void *C, hipStream_t stream) {
+    const long Ma = F6Geom::rows_pad(M), Nb = F6Geom::rows_pad(N), runs = F6Geom::runs_pad(K);
+    const uint64_t a_bytes = F6Geom::bytes(M, K), b_bytes = F6Geom::bytes(N, K);
+    void *ws = nullptr;
+    hipError_t e = stream_workspace(stream, a_bytes + b_bytes, &ws);
+    if (e != hipSuccess) return e;
+    uint8_t *w = static_cast<uint8_t *>(ws);
+    F6Prep pa{A, w, w + (size_t)Ma * runs * 16, M, (int)Ma, K, (int)runs};
+    F6Prep pb{B, w + a_bytes, w + a_bytes + (size_t)Nb * runs * 16, N, (int)Nb, K, (int)runs};
+    {
+        void *args[] = {&pa, &pb};
+        dim3 grid((unsigned)((runs + F6_PREP_RUNS - 1) / F6_PREP_RUNS),
+                  (unsigned)((Ma > Nb ? Ma : Nb) / F6_PREP_ROWS), 2);
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&s4_to_e3m2), grid, dim3(256), args, 0, stream);
+    }
+    if (e == hipSuccess) {
+        const uint8_t *ap = pa.p, *aq = pa.q, *bp = pb.p, *bq = pb.q;
+        int32_t *c = static_cast<int32_t *>(C);
+        int ma = (int)Ma, nb = (int)Nb, kt = (int)(runs / v.bkb);
+        int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
+        void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n};
+        e = hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+    }
+    return e;
 }
 
 hipError_t launch(int dtype, const Variant &v, int M, int N, int K, const void *A, const void *B,
                   void *C, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
+    if (v.kind == FP6) return launch_fp6(v, M, N, K, a, b, C, stream);
     if (v.kind == GENERIC) {
         int tiles_n = (N + 31) / 32;
         int tiles = ((M + 31) / 32) * tiles_n;
@@ -237,7 +384,7 @@ hipError_t run(int dtype, int variant, int M, int N, int K, const void *A, const
     if (M == 0 || N == 0) return hipSuccess;
     const Variant *t = table(dtype);
     if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
-    if (variant >= kNumVariants) return hipErrorInvalidValue;
+    if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
     if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
     return launch(dtype, t[variant], M, N, K, A, B, C, stream);
 }
@@ -261,11 +408,11 @@ hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, 
     return run(S4, -1, M, N, K, A, B, C, stream);
 }
 
-int mpgemm_num_variants(int dtype) { return table(dtype) ? kNumVariants : -1; }
+int mpgemm_num_variants(int dtype) { return num_variants(dtype); }
 
 const char *mpgemm_variant_name(int dtype, int variant) {
     const Variant *t = table(dtype);
-    if (!t || variant < 0 || variant >= kNumVariants) return "";
+    if (!t || variant < 0 || variant >= num_variants(dtype)) return "";
     return t[variant].name;
 }
 
@@ -279,7 +426,7 @@ int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const v
                             const void *B, const void *C) {
     const Variant *t = table(dtype);
     if (!t) return -1;
-    if (variant < 0 || variant >= kNumVariants) return 0;
+    if (variant < 0 || variant >= num_variants(dtype)) return 0;
     if (!valid_args(dtype, M, N, K, A, B, C)) return 0;
     return supports(dtype, t[variant], M, N, K, A, B, C) ? 1 : 0;
 }
@@ -288,6 +435,13 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
                               const void *B, void *C, hipStream_t stream) {
     if (variant < 0) return hipErrorInvalidValue;
     return run(dtype, variant, M, N, K, A, B, C, stream);
+}
+
+void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out) {
+    uint32_t w[4] = {0, 0, 0, 0}, o[6];
+    for (int e = 0; e < 16; ++e) w[e >> 2] |= (uint32_t)in[e] << (8 * (e & 3));
+    s4_run_to_e3m2(w, o);
+    for (int i = 0; i < 6; ++i) out[i] = o[i];
 }
 
 }  // extern "C"

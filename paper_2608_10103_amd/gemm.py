@@ -57,13 +57,15 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_variant_supports.restype = I
     L.mpgemm_run_variant.argtypes = [I, I, I, I, I, P, P, P, P]
     L.mpgemm_run_variant.restype = I
+    L.mpgemm_s4_run_to_fp6.argtypes = [P, P]
+    L.mpgemm_s4_run_to_fp6.restype = None
     _lib = L
     return L
 
 
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
                     "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
-                    "mpgemm_run_variant")
+                    "mpgemm_run_variant", "mpgemm_s4_run_to_fp6")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -173,3 +175,15 @@ def variant_supports(dtype: str, variant: int, M: int, N: int, K: int, a_ptr: in
                      b_ptr: int = 1 << 40, c_ptr: int = 1 << 44) -> bool:
     return lib().mpgemm_variant_supports(DTYPE_CODE[dtype], variant, M, N, K, a_ptr, b_ptr,
                                          c_ptr) == 1
+
+
+def s4_run_to_fp6(run: bytes) -> list:
+    """Host-side INT4 -> FP6 E3M2 conversion of one 16-byte run (32 nibbles):
+    the six 32-bit words of the 192-bit code string, code e at bits
+    [6e, 6e + 6). The same function the FP6 kernels apply on the device."""
+    if len(run) != 16:
+        raise ValueError("a run is 16 bytes")
+    src = (ctypes.c_uint8 * 16)(*run)
+    out = (ctypes.c_uint32 * 6)()
+    lib().mpgemm_s4_run_to_fp6(ctypes.addressof(src), ctypes.addressof(out))
+    return list(out)

@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2608_10103_amd as mp
@@ -33,7 +34,8 @@ def test_variant_table():
         n = mp.num_variants(dt)
         assert n >= 2
         assert mp.variant_name(dt, 0).startswith("generic")
-        assert all(mp.variant_name(dt, v).startswith(("tile", "pipe", "spread", "staged", "pingpong")) for v in range(1, n))
+        prefixes = ("tile", "pipe", "spread", "staged", "pingpong") + (("fp6pipe",) if dt == "s4" else ())
+        assert all(mp.variant_name(dt, v).startswith(prefixes) for v in range(1, n))
         assert mp.variant_name(dt, n) == ""
     assert mp.lib().mpgemm_num_variants(7) == -1
 
@@ -98,7 +100,7 @@ def test_lds_swizzle_is_conflict_free(ch):
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
-        8192: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
+        8192: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "fp6pipe256x256_w2x4_k128_s2"),
         4096: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
         2048: ("spread128x128_w2x2_k128_s4",) * 3,
         1024: ("spread128x128_w2x2_k64_s4",) * 3,
@@ -107,3 +109,51 @@ def test_selection_at_sweep_sizes():
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
         assert got == names, (n, got)
+
+
+def _e3m2_value(c):
+    """Value of a 6-bit FP6 E3M2 code from the format's definition: sign bit 5,
+    exponent bits 4..2 with bias 3, mantissa bits 1..0, subnormals at
+    exponent 0 (OCP Microscaling Formats v1.0)."""
+    sign = -1.0 if c & 0x20 else 1.0
+    e, m = (c >> 2) & 7, c & 3
+    mag = (m / 4.0) * 2.0 ** (1 - 3) if e == 0 else (1 + m / 4.0) * 2.0 ** (e - 3)
+    return sign * mag
+
+
+def test_s4_to_fp6_encoding_is_exact():
+    """Every nibble's FP6 code decodes to the nibble's two's-complement value,
+    each nibble lands in exactly one of the 32 six-bit fields, at field
+    8d + 4h + i for byte i, half h of word d (k offset 8d + 2i + h)."""
+    rng = np.random.default_rng(5)
+    runs = [bytes((2 * i) | ((2 * i + 1) << 4) for i in range(8)) * 2]  # nibbles 0..15, twice
+    runs += [rng.integers(0, 256, 16, dtype=np.uint8).tobytes() for _ in range(200)]
+    runs += [b"\x88" * 16, b"\x77" * 16, b"\x00" * 16, b"\xff" * 16]
+    for run in runs:
+        words = mp.s4_run_to_fp6(run)
+        assert len(words) == 6
+        bits = sum(int(w) << (32 * i) for i, w in enumerate(words))
+        assert bits >> 192 == 0
+        fields = set()
+        for e in range(32):
+            d, i, h = e // 8, (e % 8) // 2, e % 2
+            f = 8 * d + 4 * h + i
+            fields.add(f)
+            nib = (run[e // 2] >> (4 * (e % 2))) & 0xF
+            want = nib - 16 if nib >= 8 else nib
+            assert _e3m2_value((bits >> (6 * f)) & 0x3F) == want, (run.hex(), e)
+        assert fields == set(range(32))
+
+
+def test_fp6_variants_bound_k():
+    """The FP6 path accumulates in FP32: exact only while K (padded to 256)
+    is at most 2^18, and every such K must be accepted."""
+    fp6 = [v for v in range(mp.num_variants("s4")) if mp.variant_name("s4", v).startswith("fp6")]
+    assert fp6
+    for v in fp6:
+        assert mp.variant_supports("s4", v, 64, 64, 1 << 18)
+        assert mp.variant_supports("s4", v, 65, 3, 2)
+        assert not mp.variant_supports("s4", v, 64, 64, (1 << 18) + 2)
+        assert not mp.variant_supports("s4", v, 64, 64, 3)  # odd K is not INT4
+    for dt in ("f16", "s8"):
+        assert not any(mp.variant_name(dt, v).startswith("fp6") for v in range(mp.num_variants(dt)))

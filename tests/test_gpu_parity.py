@@ -106,7 +106,12 @@ def _variant_shapes(dtype, v):
     name = mp.variant_name(dtype, v)
     if name.startswith("generic"):
         return [(97, 65, 130), (33, 31, 66)]
-    bm, bn = (int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
+    bm, bn = (int(x) for x in re.match(r"(?:fp6)?[a-z]+(\d+)x(\d+)_", name).groups())
+    if name.startswith("fp6"):
+        # INT4 on the FP6 cores: any even K (zero-padded to whole stages)
+        k = int(name.split("_k")[1].split("_")[0])
+        return [(2 * bm, 3 * bn, 5 * k), (bm, bn, k), (2 * bm + 17, bn + 5, 3 * k + 34),
+                (1, bn - 1, 2), (bm + 31, 1, 2 * k + 6), (33, 65, 4 * k - 2)]
     kb = int(name.split("_k")[1].split("_")[0])
     elems_per_kb = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
     return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb),
@@ -325,3 +330,61 @@ def test_two_streams():
     s2.synchronize()
     assert_parity("s8", C1.cpu().numpy(), *oracle_gemm("s8", A, B), "stream 1")
     assert_parity("s4", C2.cpu().numpy(), *oracle_gemm("s4", A2, B2), "stream 2")
+
+
+# ---------------------------------------------------------------- INT4 on the FP6 matrix cores
+
+
+def _fp6_variants():
+    return [v for v in range(mp.num_variants("s4")) if mp.variant_name("s4", v).startswith("fp6")]
+
+
+def test_fp6_exact_at_the_k_limit():
+    """K = 2^18: the largest K the FP6 kernels take. All -8 sums to exactly
+    2^24 (the top of FP32's exact integer range), -8 * 7 to -56 * 2^18, and a
+    seeded random case matches the oracle bit for bit; ragged 33 x 65 tile."""
+    K = 1 << 18
+    e8 = dev(np.full((33, K // 2), 0x88, np.uint8))
+    s7 = dev(np.full((65, K // 2), 0x77, np.uint8))
+    e8b = dev(np.full((65, K // 2), 0x88, np.uint8))
+    A, B = si.gen_operands("s4", 33, 65, K, seed=2024)
+    ref = oracle.gemm_s4(A, B)
+    for v in _fp6_variants():
+        name = mp.variant_name("s4", v)
+        _log(f"fp6 K-limit {name}")
+        assert bool((mp.gemm_s4_s32(e8, e8b, variant=v) == 64 * K).all()), name
+        assert bool((mp.gemm_s4_s32(e8, s7, variant=v) == -56 * K).all()), name
+        C = gpu_gemm("s4", A, B, variant=v)
+        assert np.array_equal(C.astype(np.int64), ref), name
+
+
+def test_fp6_workspace_sizes_in_one_stream():
+    """Back-to-back FP6 calls of growing and shrinking size on one stream,
+    no synchronisation between them: each call's stream-ordered workspace
+    must not disturb the others."""
+    v = max(_fp6_variants(), key=lambda x: mp.variant_name("s4", x).startswith("fp6pipe128"))
+    cases = []
+    for i, (M, N, K) in enumerate([(512, 384, 512), (2048, 1536, 1024), (256, 128, 4096), (1024, 1024, 2050)]):
+        A, B = si.gen_operands("s4", M, N, K, seed=300 + i)
+        cases.append((A, B, mp.gemm_s4_s32(dev(A), dev(B), variant=v)))
+    torch.cuda.synchronize()
+    for A, B, C in cases:
+        assert np.array_equal(C.cpu().numpy().astype(np.int64), oracle.gemm_s4(A, B))
+
+
+def test_fp6_two_streams():
+    """Two FP6 INT4 GEMMs in flight on two streams at once."""
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    v = _fp6_variants()[0]
+    A1, B1 = si.gen_operands("s4", 2048, 2048, 2048, seed=51)
+    A2, B2 = si.gen_operands("s4", 1024, 768, 4096, seed=52)
+    d = [dev(x) for x in (A1, B1, A2, B2)]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        C1 = mp.gemm_s4_s32(d[0], d[1], stream=s1, variant=v)
+    with torch.cuda.stream(s2):
+        C2 = mp.gemm_s4_s32(d[2], d[3], stream=s2, variant=v)
+    s1.synchronize()
+    s2.synchronize()
+    assert np.array_equal(C1.cpu().numpy().astype(np.int64), oracle.gemm_s4(A1, B1))
+    assert np.array_equal(C2.cpu().numpy().astype(np.int64), oracle.gemm_s4(A2, B2))
