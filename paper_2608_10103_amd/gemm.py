@@ -179,8 +179,9 @@ def variant_supports(dtype: str, variant: int, M: int, N: int, K: int, a_ptr: in
 
 def s4_run_to_fp6(run: bytes) -> list:
     """Host-side INT4 -> FP6 E3M2 conversion of one 16-byte run (32 nibbles):
-    the six 32-bit words of the 192-bit code string, code e at bits
-    [6e, 6e + 6). The same function the FP6 kernels apply on the device."""
+    the six 32-bit words of the 192-bit code string; field f = 8d + 4h + i
+    (bits [6f, 6f + 6)) holds the code of nibble h (0 low, 1 high) of byte i
+    of 4-byte word d. The same function the FP6 kernels apply on the device."""
     if len(run) != 16:
         raise ValueError("a run is 16 bytes")
     src = (ctypes.c_uint8 * 16)(*run)
