@@ -118,6 +118,28 @@ int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const v
 hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const void *A,
                               const void *B, void *C, hipStream_t stream);
 
+/* Split-K: the pipelined variants can divide K into `splits` ranges of whole
+ * K-slices, one workgroup per (tile, range); the last workgroup of a tile to
+ * finish adds the ranges' partial sums in range order 0, 1, ... and writes C,
+ * so results do not depend on scheduling (FP16: the summation order differs
+ * from the unsplit kernel's, within the same error bound; integers: exact).
+ * Partials and per-tile counters live in a per-(device, stream) workspace
+ * like the FP6 one (allocated on first use, grown after synchronising the
+ * stream, counters zeroed on the stream when allocated, kept until the
+ * process ends). The entry points split only skinny problems (M or N at
+ * most 128) whose tile grid has fewer than 256 tiles: up to 4 ranges for
+ * FP16, 2 for the integer types. */
+
+/* Splits the entry points use for this variant and problem (1 = none), or -1
+ * for an invalid dtype, variant or size. */
+int mpgemm_select_splits(int dtype, int variant, int M, int N, int K);
+
+/* mpgemm_run_variant with an explicit split count; hipErrorInvalidValue also
+ * when the variant cannot split (only the pipelined ones can), splits < 1 or
+ * > 16, or K's slices do not divide evenly into `splits`. */
+hipError_t mpgemm_run_variant_splits(int dtype, int variant, int splits, int M, int N, int K,
+                                     const void *A, const void *B, void *C, hipStream_t stream);
+
 /* Host-side view of the INT4 -> FP6 conversion the FP6 kernels apply on the
  * device (same source): `in` is one run of 16 HOST bytes = 32 nibbles, word
  * d = bytes 4d..4d+3 (little-endian); `out` (6 words, HOST) receives a

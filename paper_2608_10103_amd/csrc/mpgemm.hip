@@ -67,33 +67,40 @@ struct Variant {
     int bm, bn, bkb;  // tile; bkb: bytes per row per K-slice (TILED), runs per stage (FP6)
     int threads;
     const void *fn;
+    bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
 };
 
 typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int);
+typedef void (*splitk_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int, int,
+                          int *, uint32_t *);
 typedef void (*generic_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int);
 
 template <int DT, class T>
 Variant tiled(const char *name) {
     kernel_fn f = &tiled_gemm<DT, T>;
-    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
 }
 
 template <int DT, class T, bool SPREAD = false>
 Variant pipelined(const char *name) {
-    kernel_fn f = &tiled_gemm_pf<DT, T, SPREAD>;
-    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+    splitk_fn f = &tiled_gemm_pf<DT, T, SPREAD>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   true};
 }
 
 template <int DT, class T, int NSETS>
 Variant staged(const char *name) {
     kernel_fn f = &tiled_gemm_rs<DT, T, NSETS>;
-    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
 }
 
 template <int DT, class T, int LEFT>
 Variant pingpong(const char *name) {
     kernel_fn f = &tiled_gemm_pp<DT, T, LEFT>;
-    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f)};
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
 }
 
 template <class T>
@@ -101,13 +108,14 @@ Variant fp6(const char *name) {
     typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
                           int32_t *, int, int, int, int, int, int, int);
     f6_fn f = &f6_gemm<T>;
-    return Variant{name, FP6, T::BM, T::BN, T::J, T::NTHREADS, reinterpret_cast<const void *>(f)};
+    return Variant{name, FP6, T::BM, T::BN, T::J, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
 }
 
 template <int DT>
 Variant generic(const char *name) {
     generic_fn f = &generic_gemm<DT>;
-    return Variant{name, GENERIC, 32, 32, 0, 64, reinterpret_cast<const void *>(f)};
+    return Variant{name, GENERIC, 32, 32, 0, 64, reinterpret_cast<const void *>(f), false};
 }
 
 #define VARIANT_LIST(DT)                                                   \
@@ -218,6 +226,10 @@ bool valid_args(int dtype, int M, int N, int K, const void *A, const void *B, co
 constexpr long kF6MaxK = 1L << 18;
 constexpr long kF6MaxRows = 65535L * 32;
 
+// Split-K buffer: kSplitCounters tile counters, then the partial tiles.
+constexpr int kSplitCounters = 16384;
+constexpr size_t kSplitCounterBytes = (size_t)kSplitCounters * 4;
+
 bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, const void *B,
               const void *C) {
     if (v.kind == GENERIC) return true;
@@ -236,6 +248,42 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
     if (dtype == S4 && K >= 131072) return false;
     if (kb > INT_MAX) return false;
     return true;
+}
+
+// Split-K (pipelined variants only): `splits` K-ranges of whole slices per
+// tile, at most kMaxSplits, the tile count within the counter block.
+constexpr int kMaxSplits = 16;
+
+long tile_count(const Variant &v, int M, int N) {
+    return (long)((M + v.bm - 1) / v.bm) * ((N + v.bn - 1) / v.bn);
+}
+
+bool splits_ok(int dtype, const Variant &v, int M, int N, int K, int splits) {
+    if (splits == 1) return true;
+    if (!v.splitk || splits < 1 || splits > kMaxSplits) return false;
+    if (tile_count(v, M, N) > kSplitCounters) return false;
+    return row_bytes(dtype, K) % ((long)v.bkb * splits) == 0;
+}
+
+// Splits the entry points use. Only skinny problems (M or N at most 128, the
+// LLM-inference shapes) are split: they stream one large operand from HBM,
+// and splitting K lets more CUs stream it. Measured on MI355X at M = 16,
+// N = K = 8192: FP16 51 -> 38 us with 4 ranges, INT8 28 -> 26 us with 2; for
+// square problems with too few tiles the fixup (partials written back to L2
+// with a device-scope release) costs more than the extra parallelism gains
+// (N = 1024: 11 -> 15 us with 2 ranges), so they are not split. Each range
+// keeps at least 8 slices.
+int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
+    if (!v.splitk || v.kind != TILED) return 1;
+    if (M > 128 && N > 128) return 1;
+    const int most = dtype == F16 ? 4 : 2;
+    const long tiles = tile_count(v, M, N);
+    const long slices = row_bytes(dtype, K) / v.bkb;
+    int s = 1;
+    while (tiles * s < 256 && 2 * s <= most && slices % (2 * s) == 0 && slices / (2 * s) >= 8 &&
+           splits_ok(dtype, v, M, N, K, 2 * s))
+        s *= 2;
+    return s;
 }
 
 // Variant indices in the tables above that the selection uses.
@@ -263,6 +311,14 @@ const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD1
 
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const Variant *t = table(dtype);
+    // Skinny problems (M or N at most 128: LLM-inference shapes) are bound by
+    // streaming the large operand from HBM; the 4-wave 128x128 pipelined
+    // kernel with split-K keeps every CU streaming, and the padding rows it
+    // computes cost MFMA time only.
+    if (M <= 128 || N <= 128) {
+        for (int cand : {V_SPREAD128_K128, V_SPREAD128_K64})
+            if (supports(dtype, t[cand], M, N, K, A, B, C)) return cand;
+    }
     const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : kPrefS4);
     const int n = dtype == F16 ? (int)(sizeof(kPrefF16) / sizeof(Pref))
                                : (dtype == S8 ? (int)(sizeof(kPrefS8) / sizeof(Pref))
@@ -273,27 +329,37 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
         // skip a tile that would mostly compute padding
         if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < n) continue;
-        if (tm * tn >= prefs[i].min_tiles) return prefs[i].variant;
+        if (tm * tn * choose_splits(dtype, v, M, N, K) >= prefs[i].min_tiles) return prefs[i].variant;
     }
     return 0;
 }
 
-// FP6 workspaces: one device buffer per (device, stream) pair, so calls on
-// one stream reuse it in stream order and calls on different streams never
-// share one. A buffer grows when a larger problem arrives: the stream is
-// synchronised first (earlier calls on it may still read the old buffer),
-// then the old buffer is freed and a larger one allocated. Buffers are kept
-// until the process ends. hipStreamPerThread names a different stream in
-// every host thread, so it is keyed by thread as well.
+// Workspaces: one device buffer per (device, stream, purpose) triple, so
+// calls on one stream reuse it in stream order and calls on different
+// streams never share one. Purposes: the FP6 operand copies and the split-K
+// counters + partials. A buffer grows when a larger problem arrives: the
+// stream is synchronised first (earlier calls on it may still use the old
+// buffer), then the old buffer is freed and a larger one allocated; a new
+// split-K buffer has its counter block zeroed on the stream (a fill kernel,
+// no memset). Buffers are kept until the process ends. hipStreamPerThread
+// names a different stream in every host thread, so it is keyed by thread
+// as well.
+enum Slot { SLOT_FP6 = 0, SLOT_SPLITK = 1 };
+
+__global__ void zero_words(uint32_t *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
 struct Workspace {
     int dev;
     hipStream_t stream;
     std::thread::id thread;
+    int slot;
     void *ptr;
     size_t bytes;
 };
 
-hipError_t stream_workspace(hipStream_t stream, size_t bytes, void **out) {
+hipError_t stream_workspace(hipStream_t stream, int slot, size_t bytes, void **out) {
     static std::mutex mu;
     static std::vector<Workspace> spaces;
     int dev = 0;
@@ -304,7 +370,7 @@ hipError_t stream_workspace(hipStream_t stream, size_t bytes, void **out) {
     std::lock_guard<std::mutex> lock(mu);
     Workspace *w = nullptr;
     for (Workspace &s : spaces)
-        if (s.dev == dev && s.stream == stream && s.thread == tid) w = &s;
+        if (s.dev == dev && s.stream == stream && s.thread == tid && s.slot == slot) w = &s;
     if (w && w->bytes >= bytes) {
         *out = w->ptr;
         return hipSuccess;
@@ -322,8 +388,19 @@ hipError_t stream_workspace(hipStream_t stream, size_t bytes, void **out) {
     void *p = nullptr;
     e = hipMalloc(&p, want);
     if (e != hipSuccess) return e;
+    if (slot == SLOT_SPLITK) {
+        uint32_t *words = static_cast<uint32_t *>(p);
+        int n = kSplitCounters;
+        void *args[] = {&words, &n};
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&zero_words), dim3(64), dim3(256), args, 0,
+                            stream);
+        if (e != hipSuccess) {
+            (void)hipFree(p);
+            return e;
+        }
+    }
     if (!w) {
-        spaces.push_back(Workspace{dev, stream, tid, nullptr, 0});
+        spaces.push_back(Workspace{dev, stream, tid, slot, nullptr, 0});
         w = &spaces.back();
     }
     w->ptr = p;
@@ -339,7 +416,7 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
     const long Ma = F6Geom::rows_pad(M), Nb = F6Geom::rows_pad(N), runs = F6Geom::runs_pad(K);
     const uint64_t a_bytes = F6Geom::bytes(M, K), b_bytes = F6Geom::bytes(N, K);
     void *ws = nullptr;
-    hipError_t e = stream_workspace(stream, a_bytes + b_bytes, &ws);
+    hipError_t e = stream_workspace(stream, SLOT_FP6, a_bytes + b_bytes, &ws);
     if (e != hipSuccess) return e;
     uint8_t *w = static_cast<uint8_t *>(ws);
     F6Prep pa{A, w, w + (size_t)Ma * runs * 16, M, (int)Ma, K, (int)runs};
@@ -361,8 +438,8 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
     return e;
 }
 
-hipError_t launch(int dtype, const Variant &v, int M, int N, int K, const void *A, const void *B,
-                  void *C, hipStream_t stream) {
+hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, const void *A,
+                  const void *B, void *C, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
     if (v.kind == FP6) return launch_fp6(v, M, N, K, a, b, C, stream);
@@ -374,19 +451,36 @@ hipError_t launch(int dtype, const Variant &v, int M, int N, int K, const void *
     }
     int kb = (int)row_bytes(dtype, K);
     int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
-    void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n};
-    return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+    if (!v.splitk) {
+        void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n};
+        return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+    }
+    int *counters = nullptr;
+    uint32_t *partials = nullptr;
+    if (splits > 1) {
+        const size_t part_bytes = (size_t)tiles_m * tiles_n * splits * v.bm * v.bn * 4;
+        void *ws = nullptr;
+        hipError_t e = stream_workspace(stream, SLOT_SPLITK, kSplitCounterBytes + part_bytes, &ws);
+        if (e != hipSuccess) return e;
+        counters = static_cast<int *>(ws);
+        partials = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + kSplitCounterBytes);
+    }
+    void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &splits, &counters, &partials};
+    return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n * splits), dim3(v.threads), args, 0, stream);
 }
 
-hipError_t run(int dtype, int variant, int M, int N, int K, const void *A, const void *B, void *C,
-               hipStream_t stream) {
+// splits < 0: the automatic choice for the variant.
+hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const void *A,
+               const void *B, void *C, hipStream_t stream) {
     if (!valid_args(dtype, M, N, K, A, B, C)) return hipErrorInvalidValue;
     if (M == 0 || N == 0) return hipSuccess;
     const Variant *t = table(dtype);
     if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
     if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
     if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
-    return launch(dtype, t[variant], M, N, K, A, B, C, stream);
+    if (splits < 0) splits = choose_splits(dtype, t[variant], M, N, K);
+    if (!splits_ok(dtype, t[variant], M, N, K, splits)) return hipErrorInvalidValue;
+    return launch(dtype, t[variant], splits, M, N, K, A, B, C, stream);
 }
 
 }  // namespace
@@ -395,17 +489,17 @@ extern "C" {
 
 hipError_t gemm_f16_f32(int M, int N, int K, const void *A, const void *B, float *C,
                         hipStream_t stream) {
-    return run(F16, -1, M, N, K, A, B, C, stream);
+    return run(F16, -1, -1, M, N, K, A, B, C, stream);
 }
 
 hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, int32_t *C,
                        hipStream_t stream) {
-    return run(S8, -1, M, N, K, A, B, C, stream);
+    return run(S8, -1, -1, M, N, K, A, B, C, stream);
 }
 
 hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
                        hipStream_t stream) {
-    return run(S4, -1, M, N, K, A, B, C, stream);
+    return run(S4, -1, -1, M, N, K, A, B, C, stream);
 }
 
 int mpgemm_num_variants(int dtype) { return num_variants(dtype); }
@@ -434,7 +528,22 @@ int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const v
 hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const void *A,
                               const void *B, void *C, hipStream_t stream) {
     if (variant < 0) return hipErrorInvalidValue;
-    return run(dtype, variant, M, N, K, A, B, C, stream);
+    return run(dtype, variant, -1, M, N, K, A, B, C, stream);
+}
+
+int mpgemm_select_splits(int dtype, int variant, int M, int N, int K) {
+    const Variant *t = table(dtype);
+    if (!t || variant < 0 || variant >= num_variants(dtype) || M < 0 || N < 0 || K < 0) return -1;
+    if (dtype == S4 && (K & 1)) return -1;
+    if (M == 0 || N == 0 || !supports(dtype, t[variant], M, N, K, nullptr, nullptr, nullptr))
+        return 1;
+    return choose_splits(dtype, t[variant], M, N, K);
+}
+
+hipError_t mpgemm_run_variant_splits(int dtype, int variant, int splits, int M, int N, int K,
+                                     const void *A, const void *B, void *C, hipStream_t stream) {
+    if (variant < 0 || splits < 1) return hipErrorInvalidValue;
+    return run(dtype, variant, splits, M, N, K, A, B, C, stream);
 }
 
 void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out) {

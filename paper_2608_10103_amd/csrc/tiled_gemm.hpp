@@ -324,12 +324,94 @@ __device__ __forceinline__ void pf_slice(uint8_t *lds, const uint8_t *const *src
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// Split-K fixup of one workgroup (see tiled_gemm_pf). Returns true in the
+// workgroup that must write C, with acc holding the sum of all splits.
+// Partial slot layout: value v of block (i, j) of thread t at word
+// ((i * FN + j) * NV + v) * NTHREADS + t of the slot, so every store and load
+// instruction covers NTHREADS consecutive words.
+template <int DT, class T>
+__device__ __forceinline__ bool splitk_fixup(typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN],
+                                             int pid, int split, int splits, int *counters,
+                                             uint32_t *partials, uint8_t *lds) {
+    typedef typename Acc<DT, T::MS>::out out_t;
+    constexpr int SLOT = T::BM * T::BN;
+    const int tid = threadIdx.x;
+    uint32_t *mine = partials + ((size_t)pid * splits + split) * SLOT;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < T::NV; ++v)
+                mine[((i * T::FN + j) * T::NV + v) * T::NTHREADS + tid] =
+                    __builtin_bit_cast(uint32_t, (out_t)acc[i][j][v]);
+    // Each wave waits until its stores have reached L2 (stores write through
+    // L1); after the barrier one thread makes them visible device-wide (the
+    // agent-scope release writes back the L2, whatever wave wrote the lines)
+    // and counts the split. Fencing in one thread instead of every wave keeps
+    // the L2 write-back / invalidate to one per workgroup.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    int *flag = reinterpret_cast<int *>(lds);
+    if (tid == 0) {
+        __threadfence();
+        const int last = atomicAdd(&counters[pid], 1) == splits - 1;
+        if (last) __threadfence();  // acquire: later loads see the other splits' partials
+        flag[0] = last;
+    }
+    __syncthreads();
+    if (!flag[0]) return false;
+    const uint32_t *tile = partials + (size_t)pid * splits * SLOT;
+    // One chunk of accumulators at a time: a block row (or, when the wave
+    // holds 256 accumulators and registers are short, one block); the loads
+    // of a chunk for one split are independent, so each split costs one memory
+    // round trip per chunk. Every element is still summed in split order.
+    constexpr int JW = (T::FM * T::FN * T::NV >= 256) ? 1 : T::FN;
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i)
+#pragma unroll
+        for (int j0 = 0; j0 < T::FN; j0 += JW) {
+#pragma unroll
+            for (int j = j0; j < j0 + JW; ++j)
+#pragma unroll
+                for (int v = 0; v < T::NV; ++v)
+                    acc[i][j][v] = __builtin_bit_cast(out_t, tile[((i * T::FN + j) * T::NV + v) * T::NTHREADS + tid]);
+            for (int s = 1; s < splits; ++s) {
+                const uint32_t *part = tile + (size_t)s * SLOT;
+                out_t add[JW][T::NV];
+#pragma unroll
+                for (int j = 0; j < JW; ++j)
+#pragma unroll
+                    for (int v = 0; v < T::NV; ++v)
+                        add[j][v] = __builtin_bit_cast(
+                            out_t, part[((i * T::FN + j0 + j) * T::NV + v) * T::NTHREADS + tid]);
+#pragma unroll
+                for (int j = 0; j < JW; ++j)
+#pragma unroll
+                    for (int v = 0; v < T::NV; ++v) acc[i][j0 + j][v] += add[j][v];
+            }
+        }
+    if (tid == 0) counters[pid] = 0;  // ready for the next call on this workspace
+    return true;
+}
+
+//
+// Split-K (splits > 1): workgroup x computes K-range x / ntiles of tile
+// x % ntiles (the K bytes divided evenly, whole slices each), stores its
+// accumulators to its slot of `partials` in register order, and counts itself
+// in counters[tile]. The workgroup that brings the count to `splits` sums the
+// tile's partials in split order 0, 1, ... (so the result does not depend on
+// which workgroup finishes last), writes C and resets the counter to zero for
+// the next call. No workgroup waits for another. The counters must be zero
+// before the first call.
 template <int DT, class T, bool SPREAD>
 __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *__restrict__ A,
                                                                const uint8_t *__restrict__ B,
                                                                void *__restrict__ Cv, int M,
                                                                int N, int Kb, int tiles_m,
-                                                               int tiles_n) {
+                                                               int tiles_n, int splits,
+                                                               int *__restrict__ counters,
+                                                               uint32_t *__restrict__ partials) {
     static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
     typedef typename Acc<DT, T::MS>::type acc_t;
     typedef typename Acc<DT, T::MS>::out out_t;
@@ -341,8 +423,13 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane % T::MS, h = lane / T::MS;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
+    const int ntiles = tiles_m * tiles_n;
+    const int split = blockIdx.x / ntiles, pid = blockIdx.x - split * ntiles;
     int tm, tn;
-    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+    tile_coords(pid, ntiles, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+    const int kb_len = Kb / splits;  // K bytes of this workgroup; a multiple of BKB
+    A += (size_t)split * kb_len;
+    B += (size_t)split * kb_len;
 
     const uint8_t *src[T::DMA_PER_WAVE];
 #pragma unroll
@@ -357,7 +444,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
 #pragma unroll
         for (int j = 0; j < T::FN; ++j) acc[i][j] = acc_t{};
 
-    const int KT = Kb / T::BKB;
+    const int KT = kb_len / T::BKB;
     // Fill the ring (all S buffers; S - 1 when later copies are spread over
     // the slices), then wait for slice 0.
     constexpr int PRE = SPREAD ? S - 1 : S;
@@ -377,6 +464,9 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
         pf_slice<DT, T, true, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
     for (; kt < KT; ++kt)
         pf_slice<DT, T, false, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
+
+    if (splits > 1 && !splitk_fixup<DT, T>(acc, pid, split, splits, counters, partials, lds))
+        return;
 
     out_t *C = reinterpret_cast<out_t *>(Cv);
     const long row0 = (long)tm * T::BM + wm * T::WTM;

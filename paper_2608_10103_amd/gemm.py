@@ -57,6 +57,10 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_variant_supports.restype = I
     L.mpgemm_run_variant.argtypes = [I, I, I, I, I, P, P, P, P]
     L.mpgemm_run_variant.restype = I
+    L.mpgemm_select_splits.argtypes = [I, I, I, I, I]
+    L.mpgemm_select_splits.restype = I
+    L.mpgemm_run_variant_splits.argtypes = [I, I, I, I, I, I, P, P, P, P]
+    L.mpgemm_run_variant_splits.restype = I
     L.mpgemm_s4_run_to_fp6.argtypes = [P, P]
     L.mpgemm_s4_run_to_fp6.restype = None
     _lib = L
@@ -65,7 +69,8 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
                     "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
-                    "mpgemm_run_variant", "mpgemm_s4_run_to_fp6")
+                    "mpgemm_run_variant", "mpgemm_select_splits", "mpgemm_run_variant_splits",
+                    "mpgemm_s4_run_to_fp6")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -103,37 +108,42 @@ def _out(dtype, M, N, A, C):
     return C
 
 
-def _call(dtype: str, A, B, C, stream, variant):
+def _call(dtype: str, A, B, C, stream, variant, splits=None):
     M, N, K = _shapes(dtype, A, B)
     C = _out(dtype, M, N, A, C)
     s = _stream_ptr(stream, A.device)
     with torch.cuda.device(A.device):
         if variant is None:
+            if splits is not None:
+                raise ValueError("splits needs an explicit variant")
             fn = getattr(lib(), {"f16": "gemm_f16_f32", "s8": "gemm_s8_s32",
                                  "s4": "gemm_s4_s32"}[dtype])
             code = fn(M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
-        else:
+        elif splits is None:
             code = lib().mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, A.data_ptr(),
                                             B.data_ptr(), C.data_ptr(), s)
+        else:
+            code = lib().mpgemm_run_variant_splits(DTYPE_CODE[dtype], variant, splits, M, N, K,
+                                                   A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
     if code != 0:
         raise HipError(code, f"{dtype} GEMM {M}x{N}x{K}")
     return C
 
 
-def gemm_f16_f32(A, B, C=None, stream=None, variant=None):
+def gemm_f16_f32(A, B, C=None, stream=None, variant=None, splits=None):
     """C = A @ B with FP16 A (M, K), FP16 B (N, K) = K x N column-major; FP32 C."""
-    return _call("f16", A, B, C, stream, variant)
+    return _call("f16", A, B, C, stream, variant, splits)
 
 
-def gemm_s8_s32(A, B, C=None, stream=None, variant=None):
+def gemm_s8_s32(A, B, C=None, stream=None, variant=None, splits=None):
     """C = A @ B with INT8 A (M, K), INT8 B (N, K); INT32 C."""
-    return _call("s8", A, B, C, stream, variant)
+    return _call("s8", A, B, C, stream, variant, splits)
 
 
-def gemm_s4_s32(A, B, C=None, stream=None, variant=None):
+def gemm_s4_s32(A, B, C=None, stream=None, variant=None, splits=None):
     """C = A @ B with packed INT4 A (M, K/2) and B (N, K/2) uint8 (low nibble =
     even k); INT32 C."""
-    return _call("s4", A, B, C, stream, variant)
+    return _call("s4", A, B, C, stream, variant, splits)
 
 
 GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
@@ -148,6 +158,11 @@ def raw_call(dtype: str, M: int, N: int, K: int, a_ptr: int, b_ptr: int, c_ptr: 
         return fn(M, N, K, a_ptr, b_ptr, c_ptr, stream_ptr)
     return L.mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, a_ptr, b_ptr, c_ptr,
                                 stream_ptr)
+
+
+def select_splits(dtype: str, variant: int, M: int, N: int, K: int) -> int:
+    """Split-K count the entry points use for this variant (1 = none)."""
+    return lib().mpgemm_select_splits(DTYPE_CODE[dtype], variant, M, N, K)
 
 
 def num_variants(dtype: str) -> int:

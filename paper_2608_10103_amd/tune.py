@@ -2,9 +2,11 @@
 
     python -m paper_2608_10103_amd.tune --dtypes f16,s8 --sizes 4096,8192 \
         --variants pipe256x256_w2x2_k128_s2,pipe256x256_w2x4_k128_s2 --rounds 7
+    python -m paper_2608_10103_amd.tune --dtypes s8 --shapes 16x8192x8192 \
+        --variants spread128 --splits 1,2,4,8
 
-For every (dtype, N) it runs each selected variant on the same seeded square
-operands, round-robin for --rounds rounds (so clock drift under power limits
+For every (dtype, shape) it runs each selected variant (and, with --splits,
+each split-K count a pipelined variant accepts) on the same seeded operands, round-robin for --rounds rounds (so clock drift under power limits
 affects all variants alike), and prints the median time per launch, TOP/s,
 the fraction of the variant's MFMA peak and whether its output equals the
 first variant's (integers) or is within 1e-3 relative of it (FP16). Variant
@@ -36,7 +38,9 @@ PEAK_FP6 = 10100.0
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--dtypes", default="f16,s8,s4")
-    ap.add_argument("--sizes", default="8192")
+    ap.add_argument("--sizes", default="8192", help="square sizes N")
+    ap.add_argument("--shapes", default="", help="MxNxK,... (added to --sizes)")
+    ap.add_argument("--splits", default="", help="split-K counts to try, e.g. 1,2,4 (default: automatic)")
     ap.add_argument("--variants", default="", help="comma-separated names or substrings")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--json", default="", help="write the results here")
@@ -44,57 +48,77 @@ def main(argv=None) -> int:
     want = [w for w in args.variants.split(",") if w]
     stream = torch.cuda.Stream()
     res = []
+    shapes = [(n, n, n) for n in (int(x) for x in args.sizes.split(",") if x)]
+    shapes += [tuple(int(x) for x in sh.split("x")) for sh in args.shapes.split(",") if sh]
+    split_list = [int(x) for x in args.splits.split(",") if x]
     for dt in args.dtypes.split(","):
-        for n in (int(x) for x in args.sizes.split(",")):
-            A, B = si.gen_operands(dt, n, n, n, seed=11)
+        for (M, N, K) in shapes:
+            A, B = si.gen_operands(dt, M, N, K, seed=11)
             Ad, Bd = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
-            vs = []
+            runs = []  # (variant, splits or None, label)
             for v in range(mp.num_variants(dt)):
                 name = mp.variant_name(dt, v)
-                if v == 0 and n > 1024:
+                if v == 0 and M * N * K > 1024 ** 3:
                     continue
                 if want and not any(w in name for w in want):
                     continue
-                if mp.variant_supports(dt, v, n, n, n, Ad.data_ptr(), Bd.data_ptr()):
-                    vs.append((v, name))
-            if not vs:
+                if not mp.variant_supports(dt, v, M, N, K, Ad.data_ptr(), Bd.data_ptr()):
+                    continue
+                if not split_list:
+                    auto = mp.select_splits(dt, v, M, N, K)
+                    runs.append((v, None, f"{name} (splits {auto})"))
+                    continue
+                for sp in split_list:
+                    C = torch.empty((M, N), dtype=torch.float32 if dt == "f16" else torch.int32, device="cuda")
+                    try:
+                        mp.GEMM[dt](Ad, Bd, C=C, variant=v, splits=sp)
+                    except mp.HipError:
+                        continue
+                    runs.append((v, sp, f"{name} splits {sp}"))
+            if not runs:
                 continue
             out_dt = torch.float32 if dt == "f16" else torch.int32
-            Cs = {v: torch.empty((n, n), dtype=out_dt, device="cuda") for v, _ in vs}
-            reps = max(2, min(40, int(1e12 / (2 * n ** 3))))
-            times = {v: [] for v, _ in vs}
+            Cs = [torch.empty((M, N), dtype=out_dt, device="cuda") for _ in runs]
+            reps = max(2, min(200, int(2e11 / (2 * M * N * K))))
+            times = [[] for _ in runs]
+
+            def call(i):
+                v, sp, _ = runs[i]
+                mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp)
+
             with torch.cuda.stream(stream):
-                for v, _ in vs:
-                    mp.GEMM[dt](Ad, Bd, C=Cs[v], stream=stream, variant=v)
+                for i in range(len(runs)):
+                    call(i)
                 for _ in range(args.rounds):
-                    for v, _ in vs:
+                    for i in range(len(runs)):
                         e0 = torch.cuda.Event(enable_timing=True)
                         e1 = torch.cuda.Event(enable_timing=True)
                         e0.record(stream)
                         for _ in range(reps):
-                            mp.GEMM[dt](Ad, Bd, C=Cs[v], stream=stream, variant=v)
+                            call(i)
                         e1.record(stream)
                         e1.synchronize()
-                        times[v].append(e0.elapsed_time(e1) / reps)
+                        times[i].append(e0.elapsed_time(e1) / reps)
             torch.cuda.synchronize()
-            ref = Cs[vs[0][0]]
-            base = float(np.median(times[vs[0][0]]))
-            for v, name in vs:
-                ms = float(np.median(times[v]))
-                tops = 2 * n ** 3 / (ms * 1e-3) / 1e12
+            ref = Cs[0]
+            base = float(np.median(times[0]))
+            for i, (v, sp, label) in enumerate(runs):
+                ms = float(np.median(times[i]))
+                tops = 2 * M * N * K / (ms * 1e-3) / 1e12
+                name = mp.variant_name(dt, v)
                 peak = PEAK_FP6 if name.startswith("fp6") else PEAK[dt]
-                if v == vs[0][0]:
+                if i == 0:
                     same = "ref"
                 elif dt == "f16":
-                    same = "close" if bool((Cs[v] - ref).abs().max() <= 1e-3 * ref.abs().max()) else "DIFFERENT"
+                    same = "close" if bool((Cs[i] - ref).abs().max() <= 1e-3 * ref.abs().max()) else "DIFFERENT"
                 else:
-                    same = "identical" if torch.equal(Cs[v], ref) else "DIFFERENT"
-                spread = 100 * (max(times[v]) - min(times[v])) / ms
-                print(f"{dt} N={n:5d} v{v:2d} {name:32s} {ms * 1e3:9.1f} us {tops:8.1f} T/s "
+                    same = "identical" if torch.equal(Cs[i], ref) else "DIFFERENT"
+                spread = 100 * (max(times[i]) - min(times[i])) / ms
+                print(f"{dt} {M}x{N}x{K} v{v:2d} {label:44s} {ms * 1e3:9.1f} us {tops:8.1f} T/s "
                       f"{100 * tops / peak:5.1f}% of peak  rel {base / ms:5.3f}  spread {spread:4.1f}%  {same}",
                       flush=True)
-                res.append(dict(dtype=dt, n=n, variant=v, name=name, us=ms * 1e3, tops=tops,
-                                frac_peak=tops / peak, rel=base / ms, check=same))
+                res.append(dict(dtype=dt, M=M, N=N, K=K, variant=v, name=name, splits=sp, us=ms * 1e3,
+                                tops=tops, frac_peak=tops / peak, rel=base / ms, check=same))
             del Cs, Ad, Bd
             torch.cuda.empty_cache()
     if args.json:

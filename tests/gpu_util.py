@@ -14,11 +14,12 @@ def dev(x: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(x)).to("cuda")
 
 
-def gpu_gemm(dtype, A, B, variant=None, stream=None):
-    """Run the dtype's entry point (or a given variant) on numpy operands;
-    returns C as numpy (float32 or int32)."""
+def gpu_gemm(dtype, A, B, variant=None, stream=None, splits=None):
+    """Run the dtype's entry point (or a given variant, optionally with an
+    explicit split-K count) on numpy operands; returns C as numpy (float32 or
+    int32)."""
     Ad, Bd = dev(A), dev(B)
-    C = mp.GEMM[dtype](Ad, Bd, variant=variant, stream=stream)
+    C = mp.GEMM[dtype](Ad, Bd, variant=variant, stream=stream, splits=splits)
     torch.cuda.synchronize()
     return C.cpu().numpy()
 

@@ -157,3 +157,25 @@ def test_fp6_variants_bound_k():
         assert not mp.variant_supports("s4", v, 64, 64, 3)  # odd K is not INT4
     for dt in ("f16", "s8"):
         assert not any(mp.variant_name(dt, v).startswith("fp6") for v in range(mp.num_variants(dt)))
+
+
+def test_split_k_selection():
+    """Only skinny problems (M or N <= 128) are split; FP16 up to 4 K-ranges,
+    integers up to 2; square sweep sizes never."""
+    for dt, most in (("f16", 4), ("s8", 2), ("s4", 2)):
+        for n in (512, 1024, 2048, 4096, 8192):
+            v = mp.select_variant(dt, n, n, n)
+            assert mp.select_splits(dt, v, n, n, n) == 1
+        for M in (1, 16, 128):
+            v = mp.select_variant(dt, M, 8192, 8192)
+            assert mp.variant_name(dt, v).startswith("spread128")
+            assert mp.select_splits(dt, v, M, 8192, 8192) == most
+            assert mp.select_splits(dt, v, 8192, M, 8192) == most
+        v = mp.select_variant(dt, 16, 8192, 1024)
+        assert mp.select_splits(dt, v, 16, 8192, 1024) <= most  # every range keeps >= 8 slices
+    assert mp.select_splits("s8", 0, 16, 8192, 8192) == 1  # the bounds-checked kernel never splits
+    L = mp.lib()
+    assert L.mpgemm_select_splits(7, 1, 16, 16, 16) == -1
+    assert L.mpgemm_select_splits(1, 999, 16, 16, 16) == -1
+    assert L.mpgemm_select_splits(1, 1, -1, 16, 16) == -1
+    assert L.mpgemm_select_splits(2, 1, 16, 16, 15) == -1  # odd K is not INT4

@@ -21,6 +21,7 @@ from tests.gpu_util import F16_TOL, assert_parity, dev, gpu_gemm, oracle_gemm
 pytestmark = pytest.mark.gpu
 
 DTYPES = ("f16", "s8", "s4")
+INVALID = 1  # hipErrorInvalidValue
 
 
 def _log(msg):
@@ -388,3 +389,84 @@ def test_fp6_two_streams():
     s2.synchronize()
     assert np.array_equal(C1.cpu().numpy().astype(np.int64), oracle.gemm_s4(A1, B1))
     assert np.array_equal(C2.cpu().numpy().astype(np.int64), oracle.gemm_s4(A2, B2))
+
+
+# ---------------------------------------------------------------- split-K and LLM-inference shapes
+
+
+def _pipelined_variants(dtype):
+    return [v for v in range(mp.num_variants(dtype))
+            if mp.variant_name(dtype, v).startswith(("pipe", "spread"))]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_splitk_every_pipelined_variant(dtype):
+    """Every split-capable variant with 2, 3 and 4 K-ranges on ragged shapes
+    spanning several tiles: bit-exact integers, FP16 within the bound."""
+    for v in _pipelined_variants(dtype):
+        name = mp.variant_name(dtype, v)
+        bm, bn = (int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
+        kb = int(name.split("_k")[1].split("_")[0])
+        e = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
+        for splits, (M, N, K) in [(2, (bm + 17, 2 * bn - 3, 4 * e)), (3, (2 * bm, bn + 1, 6 * e)),
+                                  (4, (1, bn, 8 * e)), (4, (bm - 5, 3 * bn, 4 * e))]:
+            A, B = si.gen_operands(dtype, M, N, K, seed=700 + v + splits)
+            C = gpu_gemm(dtype, A, B, variant=v, splits=splits)
+            assert_parity(dtype, C, *oracle_gemm(dtype, A, B), f"{dtype} {name} splits {splits} {M}x{N}x{K}")
+        _log(f"{dtype} split-K {name}: ok")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_llm_inference_shapes(dtype):
+    """Skinny GEMMs of LLM inference (M tokens x N outputs x K inputs) through
+    the entry point, whatever kernel and split it picks."""
+    for (M, N, K) in [(1, 4096, 4096), (16, 4096, 4096), (64, 8192, 4096), (128, 4096, 8192),
+                      (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048)]:
+        A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
+        C = gpu_gemm(dtype, A, B)
+        v = mp.select_variant(dtype, M, N, K)
+        assert_parity(dtype, C, *oracle_gemm(dtype, A, B),
+                      f"{dtype} {M}x{N}x{K} {mp.variant_name(dtype, v)} splits {mp.select_splits(dtype, v, M, N, K)}")
+    _log(f"{dtype} LLM shapes: ok")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_splitk_deterministic_and_concurrent(dtype):
+    """Split results do not depend on which workgroup finishes last (five
+    launches bit-identical), and two split-K GEMMs on two streams at once
+    keep separate workspaces."""
+    v = [x for x in _pipelined_variants(dtype) if mp.variant_name(dtype, x) == "spread128x128_w2x2_k64_s4"][0]
+    A, B = si.gen_operands(dtype, 512, 640, 2048, seed=91)
+    Ad, Bd = dev(A), dev(B)
+    first = mp.GEMM[dtype](Ad, Bd, variant=v, splits=8)
+    for _ in range(4):
+        assert torch.equal(first, mp.GEMM[dtype](Ad, Bd, variant=v, splits=8))
+    torch.cuda.synchronize()
+    assert_parity(dtype, first.cpu().numpy(), *oracle_gemm(dtype, A, B), f"{dtype} split 8")
+    A2, B2 = si.gen_operands(dtype, 384, 256, 4096, seed=92)
+    A2d, B2d = dev(A2), dev(B2)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        C1 = mp.GEMM[dtype](Ad, Bd, variant=v, splits=4, stream=s1)
+    with torch.cuda.stream(s2):
+        C2 = mp.GEMM[dtype](A2d, B2d, variant=v, splits=16, stream=s2)
+    s1.synchronize()
+    s2.synchronize()
+    assert_parity(dtype, C1.cpu().numpy(), *oracle_gemm(dtype, A, B), f"{dtype} stream 1")
+    assert_parity(dtype, C2.cpu().numpy(), *oracle_gemm(dtype, A2, B2), f"{dtype} stream 2")
+
+
+def test_splitk_argument_errors():
+    v = [x for x in _pipelined_variants("s8") if mp.variant_name("s8", x) == "spread128x128_w2x2_k64_s4"][0]
+    t = torch.zeros((256, 1024), dtype=torch.int8, device="cuda")
+    L = mp.lib()
+    c = torch.zeros((256, 256), dtype=torch.int32, device="cuda")
+    run = lambda var, sp, K: L.mpgemm_run_variant_splits(1, var, sp, 256, 256, K, t.data_ptr(), t.data_ptr(),
+                                                         c.data_ptr(), 0)
+    assert run(v, 0, 1024) == INVALID
+    assert run(v, 17, 1024) == INVALID
+    assert run(v, 3, 1024) == INVALID  # 16 slices do not split in 3
+    assert run(0, 2, 1024) == INVALID  # the bounds-checked kernel does not split
+    assert run(v, 16, 1024) == 0
+    torch.cuda.synchronize()
