@@ -91,6 +91,45 @@ hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, in
 hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
                        hipStream_t stream);
 
+/* ---- scaled outputs: the dequantisation step after the GEMM, fused ----
+ * The paper's kernels return the raw INT32 sums, without dequantisation or
+ * scaling (Scope and Generality); the next step of an inference pipeline
+ * multiplies them by per-row and per-column scales, optionally removing
+ * zero points first, and narrows the result. gemm_scaled does that in the
+ * GEMM's own epilogue:
+ *
+ *   C[i][j] = round( sa[i] * sb[j] * sum_k (A(i,k) - za[i]) * (B(k,j) - zb[j]) )
+ *
+ * with absent scales = 1 and absent zero points = 0. Integer inputs: the sum
+ * is exact (the zero-point terms are evaluated in 64-bit integers from row
+ * sums of A and column sums of B), converted to binary32 once, multiplied by
+ * sa[i] then sb[j] in binary32, and rounded to nearest even into the output
+ * type; so the result is within 1 unit in the last place of the output type
+ * of the exactly rounded value (binary32 output: within 3 ulp). FP16 inputs:
+ * the binary32 sum of the plain entry point (same error bound), scaled the
+ * same way; zero points are not accepted. The struct is a HOST pointer read
+ * during the call; the vectors it points to are DEVICE arrays of M (for _a)
+ * or N (for _b) elements, 4-byte aligned. C holds M x N elements of the
+ * output type, row-major (2-byte aligned for FP16/BF16, 4-byte for FP32).
+ * Zero points cost one extra pass over A and/or B (row sums, kept in the
+ * per-stream workspace: 4 (M + N) bytes). Errors as for the plain entry
+ * points, plus hipErrorInvalidValue for a NULL struct, an unknown output
+ * type, zero points with FP16 inputs or misaligned vectors. */
+enum { MPGEMM_OUT_F32 = 1, MPGEMM_OUT_F16 = 2, MPGEMM_OUT_BF16 = 3 };
+
+typedef struct mpgemm_epilogue {
+    const float *scale_a;  /* M per-row scales, or NULL */
+    const float *scale_b;  /* N per-column scales, or NULL */
+    const int32_t *zero_a; /* M per-row zero points (integer inputs), or NULL */
+    const int32_t *zero_b; /* N per-column zero points (integer inputs), or NULL */
+    int out_type;          /* MPGEMM_OUT_F32, MPGEMM_OUT_F16 or MPGEMM_OUT_BF16 */
+} mpgemm_epilogue;
+
+/* dtype as below (0 = FP16, 1 = INT8, 2 = INT4, same operand layouts as the
+ * plain entry points); C receives the scaled output. */
+hipError_t gemm_scaled(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                       const mpgemm_epilogue *epi, hipStream_t stream);
+
 /* ---- introspection and tuning (same operation, explicit kernel choice) ----
  * dtype: 0 = FP16->FP32, 1 = INT8->INT32, 2 = INT4->INT32. A variant is one
  * compiled kernel configuration (tile shape, wave layout, pipeline depth).
@@ -139,6 +178,11 @@ int mpgemm_select_splits(int dtype, int variant, int M, int N, int K);
  * > 16, or K's slices do not divide evenly into `splits`. */
 hipError_t mpgemm_run_variant_splits(int dtype, int variant, int splits, int M, int N, int K,
                                      const void *A, const void *B, void *C, hipStream_t stream);
+
+/* gemm_scaled with an explicit variant and split count (0 = automatic). */
+hipError_t mpgemm_run_variant_scaled(int dtype, int variant, int splits, int M, int N, int K,
+                                     const void *A, const void *B, void *C,
+                                     const mpgemm_epilogue *epi, hipStream_t stream);
 
 /* Host-side view of the INT4 -> FP6 conversion the FP6 kernels apply on the
  * device (same source): `in` is one run of 16 HOST bytes = 32 nibbles, word

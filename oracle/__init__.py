@@ -210,3 +210,79 @@ def normalized_error(C_gpu: np.ndarray, C_ref: np.ndarray, D: np.ndarray) -> flo
     if np.all(zero):
         return 0.0
     return float(np.max(err[~zero] / D[~zero]))
+
+
+# ----------------------------------------------------------------- scaled outputs
+#
+# The paper's kernels return raw sums with no dequantisation or scaling (Scope
+# and Generality). The library's scaled entry point adds that step; its
+# definition, written out here from scratch:
+#   C[i][j] = round_out( sa[i] * sb[j] * sum_k (A(i,k) - za[i]) * (B(k,j) - zb[j]) )
+# Integer inputs: the inner sum over decoded values is exact (int64 matmul of
+# the zero-point-shifted operands), the scaling is done in binary64, and the
+# result is rounded once, to nearest even, into the output format.
+
+def round_bf16(x) -> np.ndarray:
+    """Round binary64 values to the nearest bfloat16 value (1 sign, 8 exponent
+    bits with bias 127, 7 stored fraction bits), ties to even, returned as
+    binary64. Written from the format: a finite nonzero x = m * 2^e with
+    0.5 <= |m| < 1 keeps 8 significant bits, m * 2^8 rounded to an integer
+    (numpy's rint rounds halves to even); below the smallest normal (2^-126)
+    the spacing stays 2^-133; beyond the largest finite value the result is
+    infinite."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.array(x, copy=True)
+    fin = np.isfinite(x) & (x != 0)
+    m, e = np.frexp(x[fin])
+    e = np.maximum(e, -125)  # subnormal range: fixed spacing 2^(-125-8)
+    out[fin] = np.ldexp(np.rint(np.ldexp(x[fin], 8 - e)), e - 8)
+    big = np.abs(out) > float.fromhex("0x1.fep127")
+    out[big] = np.copysign(np.inf, out[big])
+    return out
+
+
+def round_out(x, out: str) -> np.ndarray:
+    """Round binary64 values to the output type ('f32', 'f16', 'bf16'), ties to
+    even, as binary64 (numpy's casts round binary64 to binary32/binary16 to
+    nearest even)."""
+    x = np.asarray(x, dtype=np.float64)
+    if out == "f32":
+        return x.astype(np.float32).astype(np.float64)
+    if out == "f16":
+        return x.astype(np.float16).astype(np.float64)
+    if out == "bf16":
+        return round_bf16(x)
+    raise ValueError(out)
+
+
+def _decoded(dtype, X):
+    """Integer operand as int64 values, one per element (rows of K)."""
+    if dtype == "s8":
+        return np.asarray(X, dtype=np.int8).astype(np.int64)
+    return s4_unpack(np.asarray(X, dtype=np.uint8)).astype(np.int64)
+
+
+def gemm_scaled(dtype, A, B, out, sa=None, sb=None, za=None, zb=None):
+    """(C_rounded, exact, D): the rounded scaled output, the binary64 value
+    before rounding, and for FP16 inputs the error scale |sa||sb| sum |a||b|
+    (None for integers). A is (M, K) row-major, B (N, K) = K x N column-major,
+    in the storage formats of gemm_f16 / gemm_s8 / gemm_s4."""
+    if dtype == "f16":
+        if za is not None or zb is not None:
+            raise ValueError("zero points apply to integer inputs only")
+        C, D = gemm_f16(A, B)
+    else:
+        a, b = _decoded(dtype, A), _decoded(dtype, B)
+        if za is not None:
+            a = a - np.asarray(za, dtype=np.int64)[:, None]
+        if zb is not None:
+            b = b - np.asarray(zb, dtype=np.int64)[:, None]
+        C = (a @ b.T).astype(np.float64)  # exact: |values| < 2^53
+        D = None
+    M, N = C.shape
+    s_a = np.ones(M) if sa is None else np.asarray(sa, dtype=np.float64)
+    s_b = np.ones(N) if sb is None else np.asarray(sb, dtype=np.float64)
+    exact = C * s_a[:, None] * s_b[None, :]
+    if D is not None:
+        D = D * np.abs(s_a)[:, None] * np.abs(s_b)[None, :]
+    return round_out(exact, out), exact, D

@@ -112,6 +112,150 @@ template <int CH> __host__ __device__ constexpr int swz(int q) {
     else return 0;
 }
 
+// ---------------------------------------------------------------------------
+// Output stage shared by every GEMM kernel. OUT_PLAIN stores the raw sum (FP32
+// for FP16 inputs, INT32 otherwise). The scaled outputs compute, per element,
+//   sa[i] * sb[j] * sum_k (A(i,k) - za[i]) (B(k,j) - zb[j])
+// (absent scales are 1, absent zero points 0; zero points only for integer
+// inputs) and store it as FP32, FP16 or BF16, rounded to nearest even. The
+// zero-point terms use the row sums of A and column sums of B:
+//   sum (a - za)(b - zb) = sum ab - zb * rowsum_a - za * colsum_b + K za zb,
+// evaluated exactly in 64-bit integers, then converted to FP32 once and
+// multiplied by the scales in FP32.
+enum Out : int { OUT_PLAIN = 0, OUT_F32 = 1, OUT_F16 = 2, OUT_BF16 = 3 };
+
+struct EpiParams {
+    const float *scale_a;  // M values or null
+    const float *scale_b;  // N values or null
+    const int *zero_a;     // M values or null
+    const int *zero_b;     // N values or null
+    const int *sum_a;      // row sums of A (used with zero_b)
+    const int *sum_b;      // column sums of B (used with zero_a)
+    int K;
+    int out;
+};
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __builtin_bit_cast(uint32_t, f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);  // NaN stays NaN
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ void store_out(const EpiParams &e, void *C, long idx, float v) {
+    if (e.out == OUT_F32) reinterpret_cast<float *>(C)[idx] = v;
+    else if (e.out == OUT_F16) reinterpret_cast<_Float16 *>(C)[idx] = (_Float16)v;
+    else reinterpret_cast<uint16_t *>(C)[idx] = f32_to_bf16_rne(v);
+}
+
+// Scaled value of one raw sum x (float for FP16 inputs, int otherwise) at
+// row i, column j, with the column terms of j preloaded.
+template <int DT, class V>
+__device__ __forceinline__ float epi_value(const EpiParams &e, V x, long i, float sb, long long zb,
+                                           long long cs) {
+    float v;
+    if constexpr (DT == F16) {
+        v = x;
+    } else {
+        long long c = x;
+        const long long za = e.zero_a ? e.zero_a[i] : 0;
+        if (e.zero_b) c -= zb * (long long)e.sum_a[i];
+        if (e.zero_a) c -= za * cs - (long long)e.K * za * zb;
+        v = (float)c;
+    }
+    if (e.scale_a) v *= e.scale_a[i];
+    return v * sb;
+}
+
+// One element (the bounds-checked kernel).
+template <int DT, class V>
+__device__ __forceinline__ void epi_store_one(const EpiParams &e, void *C, long i, long j, long N, V x) {
+    if (e.out == OUT_PLAIN) {
+        reinterpret_cast<V *>(C)[i * N + j] = x;
+        return;
+    }
+    const float sb = e.scale_b ? e.scale_b[j] : 1.0f;
+    const long long zb = e.zero_b ? e.zero_b[j] : 0, cs = e.zero_a ? e.sum_b[j] : 0;
+    store_out(e, C, i * N + j, epi_value<DT>(e, x, i, sb, zb, cs));
+}
+
+// A wave's MS x MS blocks (FM x FN of them): block (i, j) value v of lane
+// group h sits at row row0 + i MS + acc_row(h, v), column col0 + j MS (col0
+// includes the lane's column). conv maps an accumulator element to the raw
+// sum. Rows >= M and columns >= N are not stored.
+template <int DT, int MS, int FM, int FN, int NV, class AccT, class Conv>
+__device__ __forceinline__ void epi_store_tile(const EpiParams &e, void *C, const AccT (&acc)[FM][FN],
+                                               long row0, long col0, int h, int M, int N, Conv conv) {
+    typedef typename Acc<DT, MS>::out out_t;
+    if (e.out == OUT_PLAIN) {
+        out_t *Co = reinterpret_cast<out_t *>(C);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int v = 0; v < NV; ++v) {
+                    const long row = row0 + i * MS + acc_row<MS>(h, v), col = col0 + j * MS;
+                    if (row < M && col < N) Co[row * N + col] = conv(acc[i][j][v]);
+                }
+        return;
+    }
+    float sb[FN];
+    long long zb[FN], cs[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const long col = col0 + j * MS;
+        const bool ok = col < N;
+        sb[j] = (e.scale_b && ok) ? e.scale_b[col] : 1.0f;
+        zb[j] = (e.zero_b && ok) ? e.zero_b[col] : 0;
+        cs[j] = (e.zero_a && ok) ? e.sum_b[col] : 0;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const long row = row0 + i * MS + acc_row<MS>(h, v);
+            if (row >= M) continue;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const long col = col0 + j * MS;
+                if (col < N) store_out(e, C, row * N + col, epi_value<DT>(e, conv(acc[i][j][v]), row, sb[j], zb[j], cs[j]));
+            }
+        }
+}
+
+// Accumulator element -> raw sum.
+struct ConvSame {
+    template <class X> __device__ __forceinline__ X operator()(X x) const { return x; }
+};
+struct ConvShift8 {  // INT4 on the INT8 MFMA: the sums are carried times 256
+    __device__ __forceinline__ int operator()(int x) const { return x >> 8; }
+};
+struct ConvToInt {  // INT4 on the FP6 MFMA: exact integers held in FP32
+    __device__ __forceinline__ int operator()(float x) const { return (int)x; }
+};
+
+// Row sums of an integer operand stored as R rows of K values (int8 bytes or
+// packed INT4 nibbles), one block per row; used by the zero-point terms.
+template <int DT>
+__global__ __launch_bounds__(256) void row_sums(const uint8_t *__restrict__ X, int R, int K,
+                                                int *__restrict__ out) {
+    __shared__ int part[4];
+    const long kb = row_bytes(DT, K);
+    const uint8_t *row = X + (size_t)blockIdx.x * kb;
+    int s = 0;
+    for (long b = threadIdx.x; b < kb; b += 256) {
+        const uint32_t byte = row[b];
+        if constexpr (DT == S8) s += (int)(int8_t)byte;
+        else s += s4_nibble(byte, 0) + s4_nibble(byte, 1);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) out[blockIdx.x] = part[0] + part[1] + part[2] + part[3];
+}
+
 // Workgroup id -> (tile row, tile column). Workgroups are dispatched
 // round-robin over the 8 XCDs, each with its own L2; ids are first regrouped
 // so each XCD owns a contiguous run of the ordering, and the ordering walks

@@ -345,7 +345,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void f6_gemm(const uint8_t *__restr
                                                          const uint8_t *__restrict__ Bq,
                                                          int32_t *__restrict__ C, int M, int N,
                                                          int Ma, int Nb, int KT, int tiles_m,
-                                                         int tiles_n) {
+                                                         int tiles_n, EpiParams epi) {
     constexpr int S = T::STAGES;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
@@ -384,17 +384,8 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void f6_gemm(const uint8_t *__restr
 
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
-#pragma unroll
-    for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const long row = row0 + i * 32 + acc_row<32>(h, v);
-                const long col = col0 + j * 32;
-                // the sum is an integer of magnitude <= 2^24: the conversion is exact
-                if (row < M && col < N) C[row * N + col] = (int32_t)acc[i][j][v];
-            }
+    // the sums are integers of magnitude <= 2^24: the conversion is exact
+    epi_store_tile<S4, 32, T::FM, T::FN, 16>(epi, C, acc, row0, col0, h, M, N, ConvToInt());
 }
 
 }  // namespace mpg

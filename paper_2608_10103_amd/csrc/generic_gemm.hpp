@@ -18,9 +18,8 @@ template <int DT>
 __global__ __launch_bounds__(64) void generic_gemm(const uint8_t *__restrict__ A,
                                                    const uint8_t *__restrict__ B,
                                                    void *__restrict__ Cv, int M, int N, int K,
-                                                   int tiles_n) {
+                                                   int tiles_n, EpiParams epi) {
     typedef typename Acc<DT>::type acc_t;
-    typedef typename Acc<DT>::out out_t;
     const int lane = threadIdx.x;
     const int r = lane & 31, h = lane >> 5;
     const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
@@ -68,12 +67,11 @@ __global__ __launch_bounds__(64) void generic_gemm(const uint8_t *__restrict__ A
         }
     }
 
-    out_t *C = reinterpret_cast<out_t *>(Cv);
     const long ccol = (long)tn * 32 + r;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
         const long crow = (long)tm * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
-        if (crow < M && ccol < N) C[crow * N + ccol] = acc[v];
+        if (crow < M && ccol < N) epi_store_one<DT>(epi, Cv, crow, ccol, N, acc[v]);
     }
 }
 

@@ -44,6 +44,8 @@ typedef TileCfg<256, 128, 2, 2, 128, 3, 4> T256x128_w4_s3;
 typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
 typedef TileCfg<128, 128, 2, 2, 128, 4, 4> T128x128_w4_s4;
 typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
+typedef TileCfg<256, 256, 2, 4, 64, 4, 4> T256x256_w8_k64_s4;
+typedef TileCfg<256, 256, 2, 4, 64, 3, 4> T256x256_w8_k64_s3;
 
 //             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
 typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
@@ -70,10 +72,12 @@ struct Variant {
     bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
 };
 
-typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int);
+typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int,
+                          EpiParams);
 typedef void (*splitk_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int, int,
-                          int *, uint32_t *);
-typedef void (*generic_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int);
+                          int *, uint32_t *, EpiParams);
+typedef void (*generic_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int,
+                           EpiParams);
 
 template <int DT, class T>
 Variant tiled(const char *name) {
@@ -106,7 +110,7 @@ Variant pingpong(const char *name) {
 template <class T>
 Variant fp6(const char *name) {
     typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
-                          int32_t *, int, int, int, int, int, int, int);
+                          int32_t *, int, int, int, int, int, int, int, EpiParams);
     f6_fn f = &f6_gemm<T>;
     return Variant{name, FP6, T::BM, T::BN, T::J, T::NTHREADS, reinterpret_cast<const void *>(f),
                    false};
@@ -152,7 +156,9 @@ Variant generic(const char *name) {
      pingpong<DT, T256x256_w8_s2, 2>("pingpong256x256_k128_c2"),          \
      pingpong<DT, T256x256_w8_s2, 6>("pingpong256x256_k128_c6"),          \
      pingpong<DT, T256x256_w8_k64_s2, 4>("pingpong256x256_k64_c4"),       \
-     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16")
+     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16"), \
+     pipelined<DT, T256x256_w8_k64_s4>("pipe256x256_w2x4_k64_s4"),          \
+     pipelined<DT, T256x256_w8_k64_s3>("pipe256x256_w2x4_k64_s3")
 
 const Variant kF16[] = {VARIANT_LIST(F16)};
 const Variant kS8[] = {VARIANT_LIST(S8)};
@@ -197,22 +203,24 @@ bool overlap(const void *p, uint64_t n, const void *q, uint64_t m) {
     return a < b + m && b < a + n;
 }
 
-// Argument checks shared by every entry point (see the header's Errors).
-bool valid_args(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
+// Argument checks shared by every entry point (see the header's Errors);
+// c_elem = bytes per element of C (4, or 2 for FP16/BF16 scaled outputs).
+bool valid_args(int dtype, int M, int N, int K, const void *A, const void *B, const void *C,
+                int c_elem = 4) {
     if (dtype < F16 || dtype > S4) return false;
     if (M < 0 || N < 0 || K < 0) return false;
     if (K > INT_MAX - 64) return false;
     if (dtype == S4 && (K & 1)) return false;
     if (M == 0 || N == 0) return true;
-    if (!C || !aligned(C, 4)) return false;
+    if (!C || !aligned(C, (uintptr_t)c_elem)) return false;
     if (K > 0) {
         if (!A || !B) return false;
         if (dtype == F16 && (!aligned(A, 2) || !aligned(B, 2))) return false;
     }
     const uint64_t rb = (uint64_t)row_bytes(dtype, K);
     const uint64_t a_bytes = (uint64_t)M * rb, b_bytes = (uint64_t)N * rb;
-    const uint64_t c_bytes = (uint64_t)M * (uint64_t)N * 4u;
-    if (c_bytes / 4u / (uint64_t)N != (uint64_t)M) return false;
+    const uint64_t c_bytes = (uint64_t)M * (uint64_t)N * (uint64_t)c_elem;
+    if (c_bytes / (uint64_t)c_elem / (uint64_t)N != (uint64_t)M) return false;
     if (uintptr_t(-1) - reinterpret_cast<uintptr_t>(C) < c_bytes) return false;
     if (K > 0 && (overlap(C, c_bytes, A, a_bytes) || overlap(C, c_bytes, B, b_bytes))) return false;
     // the bounds-checked kernel indexes tiles with a 32-bit grid
@@ -237,13 +245,12 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
     if (v.kind == FP6) {
         if (dtype != S4) return false;
         if (F6Geom::runs_pad(K) * 32 > kF6MaxK) return false;
-        if (F6Geom::rows_pad(M) > kF6MaxRows || F6Geom::rows_pad(N) > kF6MaxRows) return false;
-        return aligned(C, 4);
+        return F6Geom::rows_pad(M) <= kF6MaxRows && F6Geom::rows_pad(N) <= kF6MaxRows;
     }
     const long kb = row_bytes(dtype, K);
     // edge tiles are predicated in M and N; K must fill whole slices
     if (kb % v.bkb) return false;
-    if (!aligned(A, 16) || !aligned(B, 16) || !aligned(C, 4)) return false;
+    if (!aligned(A, 16) || !aligned(B, 16)) return false;
     // INT4 partial sums are carried scaled by 256 (see s4_lo_x16)
     if (dtype == S4 && K >= 131072) return false;
     if (kb > INT_MAX) return false;
@@ -293,8 +300,9 @@ enum : int {
     V_SPREAD128_K64 = 21,    // spread128x128_w2x2_k64_s4
     V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
     V_PIPE64 = 13,           // pipe64x64_w1x1_k128_s4
-    V_FP6_256_S2 = 35,       // fp6pipe256x256_w2x4_k128_s2 (INT4 only)
 };
+// INT4-only variants follow the common list in kS4.
+constexpr int V_FP6_256_S2 = kNumF16 + 1;  // fp6pipe256x256_w2x4_k128_s2
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
 // taken when it supports the problem and yields at least `min_tiles`
@@ -336,15 +344,15 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
 
 // Workspaces: one device buffer per (device, stream, purpose) triple, so
 // calls on one stream reuse it in stream order and calls on different
-// streams never share one. Purposes: the FP6 operand copies and the split-K
-// counters + partials. A buffer grows when a larger problem arrives: the
+// streams never share one. Purposes: the FP6 operand copies, the split-K
+// counters + partials, and the row sums the zero-point epilogue needs. A buffer grows when a larger problem arrives: the
 // stream is synchronised first (earlier calls on it may still use the old
 // buffer), then the old buffer is freed and a larger one allocated; a new
 // split-K buffer has its counter block zeroed on the stream (a fill kernel,
 // no memset). Buffers are kept until the process ends. hipStreamPerThread
 // names a different stream in every host thread, so it is keyed by thread
 // as well.
-enum Slot { SLOT_FP6 = 0, SLOT_SPLITK = 1 };
+enum Slot { SLOT_FP6 = 0, SLOT_SPLITK = 1, SLOT_SUMS = 2 };
 
 __global__ void zero_words(uint32_t *p, int n) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
@@ -412,7 +420,7 @@ hipError_t stream_workspace(hipStream_t stream, int slot, size_t bytes, void **o
 // INT4 on the FP6 matrix cores: convert both operands into the stream's
 // workspace, then run the FP6 tile kernel.
 hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, const uint8_t *B,
-                      void *C, hipStream_t stream) {
+                      void *C, EpiParams epi, hipStream_t stream) {
     const long Ma = F6Geom::rows_pad(M), Nb = F6Geom::rows_pad(N), runs = F6Geom::runs_pad(K);
     const uint64_t a_bytes = F6Geom::bytes(M, K), b_bytes = F6Geom::bytes(N, K);
     void *ws = nullptr;
@@ -432,27 +440,27 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
         int32_t *c = static_cast<int32_t *>(C);
         int ma = (int)Ma, nb = (int)Nb, kt = (int)(runs / v.bkb);
         int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
-        void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n};
+        void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &epi};
         e = hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
     return e;
 }
 
 hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, const void *A,
-                  const void *B, void *C, hipStream_t stream) {
+                  const void *B, void *C, EpiParams epi, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
-    if (v.kind == FP6) return launch_fp6(v, M, N, K, a, b, C, stream);
+    if (v.kind == FP6) return launch_fp6(v, M, N, K, a, b, C, epi, stream);
     if (v.kind == GENERIC) {
         int tiles_n = (N + 31) / 32;
         int tiles = ((M + 31) / 32) * tiles_n;
-        void *args[] = {&a, &b, &C, &M, &N, &K, &tiles_n};
+        void *args[] = {&a, &b, &C, &M, &N, &K, &tiles_n, &epi};
         return hipLaunchKernel(v.fn, dim3(tiles), dim3(v.threads), args, 0, stream);
     }
     int kb = (int)row_bytes(dtype, K);
     int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
     if (!v.splitk) {
-        void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n};
+        void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &epi};
         return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
     int *counters = nullptr;
@@ -465,14 +473,65 @@ hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, 
         counters = static_cast<int *>(ws);
         partials = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + kSplitCounterBytes);
     }
-    void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &splits, &counters, &partials};
+    void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &splits, &counters, &partials, &epi};
     return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n * splits), dim3(v.threads), args, 0, stream);
 }
 
-// splits < 0: the automatic choice for the variant.
+// Row sums for the zero-point terms into the stream's sums workspace.
+hipError_t zero_point_sums(int dtype, int M, int N, int K, const void *A, const void *B,
+                           EpiParams &epi, hipStream_t stream) {
+    if (!epi.zero_a && !epi.zero_b) return hipSuccess;
+    void *ws = nullptr;
+    hipError_t e = stream_workspace(stream, SLOT_SUMS, ((size_t)M + N) * 4, &ws);
+    if (e != hipSuccess) return e;
+    int *sums = static_cast<int *>(ws);
+    const void *fn = dtype == S8 ? reinterpret_cast<const void *>(&row_sums<S8>)
+                                 : reinterpret_cast<const void *>(&row_sums<S4>);
+    if (epi.zero_b) {  // needs the row sums of A
+        const uint8_t *x = static_cast<const uint8_t *>(A);
+        int r = M, k = K;
+        int *out = sums;
+        void *args[] = {&x, &r, &k, &out};
+        e = hipLaunchKernel(fn, dim3(M), dim3(256), args, 0, stream);
+        if (e != hipSuccess) return e;
+        epi.sum_a = out;
+    }
+    if (epi.zero_a) {  // needs the column sums of B (rows of its N x K storage)
+        const uint8_t *x = static_cast<const uint8_t *>(B);
+        int r = N, k = K;
+        int *out = sums + M;
+        void *args[] = {&x, &r, &k, &out};
+        e = hipLaunchKernel(fn, dim3(N), dim3(256), args, 0, stream);
+        if (e != hipSuccess) return e;
+        epi.sum_b = out;
+    }
+    return hipSuccess;
+}
+
+EpiParams plain_epilogue(int K) { return EpiParams{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, K, OUT_PLAIN}; }
+
+// Scaled-output arguments: a known output type; zero points only for integer
+// inputs; scale and zero-point vectors 4-byte aligned.
+bool valid_epilogue(int dtype, const mpgemm_epilogue *e) {
+    if (!e) return false;
+    if (e->out_type != MPGEMM_OUT_F32 && e->out_type != MPGEMM_OUT_F16 && e->out_type != MPGEMM_OUT_BF16)
+        return false;
+    if (dtype == F16 && (e->zero_a || e->zero_b)) return false;
+    for (const void *p : {(const void *)e->scale_a, (const void *)e->scale_b, (const void *)e->zero_a,
+                          (const void *)e->zero_b})
+        if (p && !aligned(p, 4)) return false;
+    return true;
+}
+
+// variant < 0: the selection; splits < 0: the automatic choice for the variant.
 hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const void *A,
-               const void *B, void *C, hipStream_t stream) {
-    if (!valid_args(dtype, M, N, K, A, B, C)) return hipErrorInvalidValue;
+               const void *B, void *C, hipStream_t stream, const mpgemm_epilogue *scaled = nullptr) {
+    int c_elem = 4;
+    if (scaled) {
+        if (dtype < F16 || dtype > S4 || !valid_epilogue(dtype, scaled)) return hipErrorInvalidValue;
+        c_elem = scaled->out_type == MPGEMM_OUT_F32 ? 4 : 2;
+    }
+    if (!valid_args(dtype, M, N, K, A, B, C, c_elem)) return hipErrorInvalidValue;
     if (M == 0 || N == 0) return hipSuccess;
     const Variant *t = table(dtype);
     if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
@@ -480,7 +539,17 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
     if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
     if (splits < 0) splits = choose_splits(dtype, t[variant], M, N, K);
     if (!splits_ok(dtype, t[variant], M, N, K, splits)) return hipErrorInvalidValue;
-    return launch(dtype, t[variant], splits, M, N, K, A, B, C, stream);
+    EpiParams epi = plain_epilogue(K);
+    if (scaled) {
+        epi.scale_a = scaled->scale_a;
+        epi.scale_b = scaled->scale_b;
+        epi.zero_a = scaled->zero_a;
+        epi.zero_b = scaled->zero_b;
+        epi.out = scaled->out_type;
+        const hipError_t e = zero_point_sums(dtype, M, N, K, A, B, epi, stream);
+        if (e != hipSuccess) return e;
+    }
+    return launch(dtype, t[variant], splits, M, N, K, A, B, C, epi, stream);
 }
 
 }  // namespace
@@ -551,6 +620,19 @@ void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out) {
     for (int e = 0; e < 16; ++e) w[e >> 2] |= (uint32_t)in[e] << (8 * (e & 3));
     s4_run_to_e3m2(w, o);
     for (int i = 0; i < 6; ++i) out[i] = o[i];
+}
+
+hipError_t gemm_scaled(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                       const mpgemm_epilogue *epi, hipStream_t stream) {
+    if (!epi) return hipErrorInvalidValue;
+    return run(dtype, -1, -1, M, N, K, A, B, C, stream, epi);
+}
+
+hipError_t mpgemm_run_variant_scaled(int dtype, int variant, int splits, int M, int N, int K,
+                                     const void *A, const void *B, void *C,
+                                     const mpgemm_epilogue *epi, hipStream_t stream) {
+    if (variant < 0 || splits < 0 || !epi) return hipErrorInvalidValue;
+    return run(dtype, variant, splits == 0 ? -1 : splits, M, N, K, A, B, C, stream, epi);
 }
 
 }  // extern "C"

@@ -411,10 +411,10 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
                                                                int N, int Kb, int tiles_m,
                                                                int tiles_n, int splits,
                                                                int *__restrict__ counters,
-                                                               uint32_t *__restrict__ partials) {
+                                                               uint32_t *__restrict__ partials,
+                                                               EpiParams epi) {
     static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
     typedef typename Acc<DT, T::MS>::type acc_t;
-    typedef typename Acc<DT, T::MS>::out out_t;
     constexpr int S = T::STAGES;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
@@ -468,22 +468,12 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
     if (splits > 1 && !splitk_fixup<DT, T>(acc, pid, split, splits, counters, partials, lds))
         return;
 
-    out_t *C = reinterpret_cast<out_t *>(Cv);
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
-#pragma unroll
-    for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < T::NV; ++v) {
-                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
-                const long col = col0 + j * T::MS;
-                if (row < M && col < N) {
-                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                    else C[row * N + col] = acc[i][j][v];
-                }
-            }
+    if constexpr (DT == S4)
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvShift8());
+    else
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
 }
 
 // ---------------------------------------------------------------------------
@@ -621,11 +611,10 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *_
                                                                const uint8_t *__restrict__ B,
                                                                void *__restrict__ Cv, int M,
                                                                int N, int Kb, int tiles_m,
-                                                               int tiles_n) {
+                                                               int tiles_n, EpiParams epi) {
     static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
     static_assert(NSETS == 1 || NSETS == 2, "one or two register sets in flight");
     typedef typename Acc<DT, T::MS>::type acc_t;
-    typedef typename Acc<DT, T::MS>::out out_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
@@ -676,22 +665,12 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_rs(const uint8_t *_
             rs_slice<DT, T, 1, 2>(lds, src, wave, lane, kt, KT, wm, wn, r, h, stg, ra, rb, acc);
     }
 
-    out_t *C = reinterpret_cast<out_t *>(Cv);
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
-#pragma unroll
-    for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < T::NV; ++v) {
-                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
-                const long col = col0 + j * T::MS;
-                if (row < M && col < N) {
-                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                    else C[row * N + col] = acc[i][j][v];
-                }
-            }
+    if constexpr (DT == S4)
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvShift8());
+    else
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
 }
 
 // ---------------------------------------------------------------------------
@@ -793,12 +772,11 @@ template <int DT, class T, int LEFT>
 __global__ __launch_bounds__(512, 1) void tiled_gemm_pp(const uint8_t *__restrict__ A,
                                                        const uint8_t *__restrict__ B,
                                                        void *__restrict__ Cv, int M, int N, int Kb,
-                                                       int tiles_m, int tiles_n) {
+                                                       int tiles_m, int tiles_n, EpiParams epi) {
     typedef PingPong<T> P;
     static_assert(T::NTHREADS == 512, "8 waves");
     static_assert(LEFT >= 1 && LEFT < T::FM * T::FN, "carried MFMA blocks");
     typedef typename Acc<DT, T::MS>::type acc_t;
-    typedef typename Acc<DT, T::MS>::out out_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
@@ -871,31 +849,20 @@ __global__ __launch_bounds__(512, 1) void tiled_gemm_pp(const uint8_t *__restric
     // group 0's last phase, matching the barrier of group 1's last compute
     if (g == 0) wait_vm_barrier<63>();
 
-    out_t *C = reinterpret_cast<out_t *>(Cv);
     const long row0 = (long)tm * T::BM + g * T::WTM;
     const long col0 = (long)tn * T::BN + w4 * T::WTN + r;
-#pragma unroll
-    for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < T::NV; ++v) {
-                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
-                const long col = col0 + j * T::MS;
-                if (row < M && col < N) {
-                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                    else C[row * N + col] = acc[i][j][v];
-                }
-            }
+    if constexpr (DT == S4)
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvShift8());
+    else
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
 }
 
 template <int DT, class T>
 __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__restrict__ A,
                                                             const uint8_t *__restrict__ B,
                                                             void *__restrict__ Cv, int M, int N,
-                                                            int Kb, int tiles_m, int tiles_n) {
+                                                            int Kb, int tiles_m, int tiles_n, EpiParams epi) {
     typedef typename Acc<DT, T::MS>::type acc_t;
-    typedef typename Acc<DT, T::MS>::out out_t;
     __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
 
     const int tid = threadIdx.x;
@@ -933,22 +900,12 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm(const uint8_t *__re
         compute_stage<DT, T>(lds + (kt % T::STAGES) * T::STAGE_BYTES, wm, wn, r, h, acc);
     }
 
-    out_t *C = reinterpret_cast<out_t *>(Cv);
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
-#pragma unroll
-    for (int i = 0; i < T::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < T::NV; ++v) {
-                const long row = row0 + i * T::MS + acc_row<T::MS>(h, v);
-                const long col = col0 + j * T::MS;
-                if (row < M && col < N) {
-                    if constexpr (DT == S4) C[row * N + col] = acc[i][j][v] >> 8;
-                    else C[row * N + col] = acc[i][j][v];
-                }
-            }
+    if constexpr (DT == S4)
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvShift8());
+    else
+        epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
 }
 
 }  // namespace mpg

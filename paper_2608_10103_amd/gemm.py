@@ -61,6 +61,10 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_select_splits.restype = I
     L.mpgemm_run_variant_splits.argtypes = [I, I, I, I, I, I, P, P, P, P]
     L.mpgemm_run_variant_splits.restype = I
+    L.gemm_scaled.argtypes = [I, I, I, I, P, P, P, P, P]
+    L.gemm_scaled.restype = I
+    L.mpgemm_run_variant_scaled.argtypes = [I, I, I, I, I, I, P, P, P, P, P]
+    L.mpgemm_run_variant_scaled.restype = I
     L.mpgemm_s4_run_to_fp6.argtypes = [P, P]
     L.mpgemm_s4_run_to_fp6.restype = None
     _lib = L
@@ -70,7 +74,7 @@ def lib() -> ctypes.CDLL:
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
                     "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
                     "mpgemm_run_variant", "mpgemm_select_splits", "mpgemm_run_variant_splits",
-                    "mpgemm_s4_run_to_fp6")
+                    "gemm_scaled", "mpgemm_run_variant_scaled", "mpgemm_s4_run_to_fp6")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -147,6 +151,56 @@ def gemm_s4_s32(A, B, C=None, stream=None, variant=None, splits=None):
 
 
 GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
+
+
+class Epilogue(ctypes.Structure):
+    """mpgemm_epilogue of include/mpgemm.h (device pointers, output type)."""
+    _fields_ = [("scale_a", ctypes.c_void_p), ("scale_b", ctypes.c_void_p),
+                ("zero_a", ctypes.c_void_p), ("zero_b", ctypes.c_void_p), ("out_type", ctypes.c_int)]
+
+
+OUT_TYPE = {torch.float32: 1, torch.float16: 2, torch.bfloat16: 3}
+
+
+def _vec(x, n, dtype, name, device):
+    if x is None:
+        return None
+    if x.dtype != dtype or x.dim() != 1 or x.numel() != n or not x.is_contiguous() or x.device != device:
+        raise ValueError(f"{name} must be a contiguous ({n},) {dtype} tensor on {device}")
+    return x.data_ptr()
+
+
+def gemm_scaled(dtype: str, A, B, scale_a=None, scale_b=None, zero_a=None, zero_b=None,
+                out_dtype=torch.float16, C=None, stream=None, variant=None, splits=None):
+    """C = round(scale_a[i] * scale_b[j] * sum_k (A(i,k) - zero_a[i]) (B(k,j) - zero_b[j]))
+    in out_dtype (float32, float16 or bfloat16); operands as for GEMM[dtype];
+    scales float32 (M,) / (N,), zero points int32 (M,) / (N,) (integer inputs
+    only), any of them None. Runs in the GEMM kernels' epilogue."""
+    M, N, K = _shapes(dtype, A, B)
+    if out_dtype not in OUT_TYPE:
+        raise ValueError("out_dtype must be float32, float16 or bfloat16")
+    dev = A.device
+    epi = Epilogue(_vec(scale_a, M, torch.float32, "scale_a", dev), _vec(scale_b, N, torch.float32, "scale_b", dev),
+                   _vec(zero_a, M, torch.int32, "zero_a", dev), _vec(zero_b, N, torch.int32, "zero_b", dev),
+                   OUT_TYPE[out_dtype])
+    if C is None:
+        C = torch.empty((M, N), dtype=out_dtype, device=dev)
+    elif C.dtype != out_dtype or tuple(C.shape) != (M, N) or not C.is_contiguous() or C.device != dev:
+        raise ValueError(f"C must be a contiguous ({M}, {N}) {out_dtype} tensor on {dev}")
+    s = _stream_ptr(stream, dev)
+    with torch.cuda.device(dev):
+        if variant is None:
+            if splits is not None:
+                raise ValueError("splits needs an explicit variant")
+            code = lib().gemm_scaled(DTYPE_CODE[dtype], M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                     ctypes.addressof(epi), s)
+        else:
+            code = lib().mpgemm_run_variant_scaled(DTYPE_CODE[dtype], variant, splits or 0, M, N, K,
+                                                   A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                                   ctypes.addressof(epi), s)
+    if code != 0:
+        raise HipError(code, f"scaled {dtype} GEMM {M}x{N}x{K}")
+    return C
 
 
 def raw_call(dtype: str, M: int, N: int, K: int, a_ptr: int, b_ptr: int, c_ptr: int,

@@ -46,3 +46,33 @@ def assert_parity(dtype, C_gpu, C_ref, D, what=""):
     assert bad.size == 0, (f"{what}: {len(bad)} mismatches, first at {tuple(bad[0])}: "
                            f"gpu {C_gpu[tuple(bad[0])]} oracle {C_ref[tuple(bad[0])]}")
     return 0.0
+
+
+# Output formats of the scaled entry point: (stored fraction bits, minimum
+# normal exponent).
+_FORMATS = {"f32": (23, -126), "f16": (10, -14), "bf16": (7, -126)}
+TORCH_OUT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+
+def ulp_of(x, out):
+    """Spacing of the output format at |x| (the subnormal spacing below the
+    smallest normal)."""
+    frac, emin = _FORMATS[out]
+    ax = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), 2.0 ** emin)
+    return np.ldexp(1.0, (np.floor(np.log2(ax)).astype(np.int64) - frac))
+
+
+def assert_scaled(got, exact, D, out, what=""):
+    """Scaled outputs: the GPU scales in binary32 (at most 3 roundings before
+    the output rounding), so a result may sit one output ulp from the
+    correctly rounded value: |got - exact| <= 1 ulp (binary32 output: 4 ulp).
+    FP16 inputs add the sum's bound 1e-3 * D (D already scaled)."""
+    g = got.float().cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(g)), f"{what}: non-finite output"
+    tol = ulp_of(exact, out) * (4.0 if out == "f32" else 1.0)
+    if D is not None:
+        tol = tol + F16_TOL * D + 2.0 ** -21 * np.abs(exact)
+    err = np.abs(g - exact)
+    bad = err > tol
+    assert not np.any(bad), (f"{what}: {int(bad.sum())} elements off, worst at "
+                             f"{np.unravel_index(np.argmax(err - tol), err.shape)}")

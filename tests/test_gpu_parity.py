@@ -7,6 +7,7 @@ compiled kernel variant on shapes spanning several tiles, closed forms and
 edge cases. Integer results must match bit for bit; FP16 within a normalised
 error of 1e-3.
 """
+import ctypes
 import re
 
 import numpy as np
@@ -469,4 +470,88 @@ def test_splitk_argument_errors():
     assert run(v, 3, 1024) == INVALID  # 16 slices do not split in 3
     assert run(0, 2, 1024) == INVALID  # the bounds-checked kernel does not split
     assert run(v, 16, 1024) == 0
+    torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- scaled outputs (fused epilogue)
+
+from tests.gpu_util import TORCH_OUT, assert_scaled  # noqa: E402
+
+OUTS = ("f32", "f16", "bf16")
+
+
+def _scales(dtype, M, N, seed, zero_points):
+    """Seeded scales that keep outputs inside FP16's range, optional zero points."""
+    rng = np.random.default_rng(seed)
+    lo, hi = {"f16": (0.5, 2.0), "s8": (2.0 ** -14, 2.0 ** -10), "s4": (2.0 ** -8, 2.0 ** -4)}[dtype]
+    sa = rng.uniform(lo, hi, M).astype(np.float32)
+    sb = rng.uniform(0.5, 2.0, N).astype(np.float32)
+    za = zb = None
+    if zero_points:
+        r = 8 if dtype == "s8" else 3
+        za = rng.integers(-r, r + 1, M).astype(np.int32)
+        zb = rng.integers(-r, r + 1, N).astype(np.int32)
+    return sa, sb, za, zb
+
+
+def _run_scaled(dtype, A, B, out, sa, sb, za, zb, variant=None, splits=None):
+    t = lambda x: None if x is None else dev(x)
+    C = mp.gemm_scaled(dtype, dev(A), dev(B), t(sa), t(sb), t(za), t(zb), out_dtype=TORCH_OUT[out],
+                       variant=variant, splits=splits)
+    torch.cuda.synchronize()
+    return C
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_scaled_epilogue_every_kernel(dtype):
+    """Every kernel variant's epilogue with scales (and, for integers, zero
+    points on every other variant), output types in rotation, on a ragged
+    shape spanning several tiles."""
+    for v in range(mp.num_variants(dtype)):
+        M, N, K = _variant_shapes(dtype, v)[-1 if v == 0 else 3]
+        out = OUTS[v % 3]
+        zp = dtype != "f16" and v % 2 == 1
+        A, B = si.gen_operands(dtype, M, N, K, seed=1500 + v)
+        sa, sb, za, zb = _scales(dtype, M, N, 1600 + v, zp)
+        C = _run_scaled(dtype, A, B, out, sa, sb, za, zb, variant=v)
+        _, exact, D = oracle.gemm_scaled(dtype, A, B, out, sa, sb, za, zb)
+        assert_scaled(C, exact, D, out, f"{dtype} {mp.variant_name(dtype, v)} {M}x{N}x{K} {out} zp={zp}")
+    _log(f"{dtype} scaled epilogue, every variant: ok")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("out", OUTS)
+def test_scaled_entry_point(dtype, out):
+    """Through gemm_scaled with the library's own kernel choice: a square tiled
+    problem, a skinny split-K one, one-sided scales and zero points."""
+    for i, (M, N, K, zp, one_sided) in enumerate([(512, 640, 1024, False, False), (16, 2048, 4096, True, False),
+                                                   (300, 257, 512, True, True), (64, 64, 0, True, False)]):
+        zp = zp and dtype != "f16"
+        A, B = si.gen_operands(dtype, M, N, K, seed=1700 + i)
+        sa, sb, za, zb = _scales(dtype, M, N, 1800 + i, zp)
+        if one_sided:
+            sb, za = None, None
+        C = _run_scaled(dtype, A, B, out, sa, sb, za, zb)
+        _, exact, D = oracle.gemm_scaled(dtype, A, B, out, sa, sb, za, zb)
+        assert_scaled(C, exact, D, out, f"{dtype} {M}x{N}x{K} {out}")
+
+
+def test_scaled_argument_errors():
+    L = mp.lib()
+    t = torch.zeros((64, 64), dtype=torch.int8, device="cuda")
+    h = torch.zeros((64, 64), dtype=torch.float16, device="cuda")
+    c = torch.zeros((64, 64), dtype=torch.float16, device="cuda")
+    s = torch.ones(64, dtype=torch.float32, device="cuda")
+    z = torch.zeros(64, dtype=torch.int32, device="cuda")
+    E = mp.gemm.Epilogue
+    call = lambda dt, A, epi, cptr=c.data_ptr(): L.gemm_scaled(dt, 64, 64, 64, A.data_ptr(), A.data_ptr(), cptr,
+                                                               None if epi is None else ctypes.addressof(epi), 0)
+    assert call(1, t, None) == INVALID
+    assert call(1, t, E(s.data_ptr(), None, None, None, 0)) == INVALID      # no output type
+    assert call(1, t, E(s.data_ptr(), None, None, None, 4)) == INVALID      # unknown output type
+    assert call(0, h, E(None, None, z.data_ptr(), None, 2)) == INVALID      # zero points with FP16
+    assert call(1, t, E(s.data_ptr() + 2, None, None, None, 2)) == INVALID  # misaligned scales
+    assert call(1, t, E(None, None, None, None, 1), c.data_ptr() + 2) == INVALID  # FP32 output: 4-byte C
+    assert call(1, t, E(None, None, None, None, 2), c.data_ptr() + 1) == INVALID  # FP16 output: 2-byte C
+    assert call(1, t, E(s.data_ptr(), s.data_ptr(), z.data_ptr(), z.data_ptr(), 3)) == 0
     torch.cuda.synchronize()

@@ -300,3 +300,67 @@ def test_pins_catch_mutants(name, tmp_path):
         except (AssertionError, ValueError, IndexError):
             failed.append(pin.__name__)
     assert failed, f"mutant {name} passed every pin"
+
+
+# ---------------------------------------------------------------- scaled outputs
+
+
+def _rne_exact(x, frac_bits, emin):
+    """x rounded to frac_bits stored fraction bits (ties to even), exponent
+    floor emin (fixed spacing below the smallest normal), in exact rationals."""
+    from fractions import Fraction
+    if x == 0:
+        return 0.0
+    f = abs(Fraction(x))
+    e = 0
+    while f >= 2:
+        f /= 2
+        e += 1
+    while f < 1:
+        f *= 2
+        e -= 1
+    scale = Fraction(2) ** (max(e, emin) - frac_bits)
+    q = Fraction(x) / scale
+    n = q.numerator // q.denominator
+    r = q - n
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return float(n * scale)
+
+
+def test_round_bf16_matches_exact_rounding():
+    rng = np.random.default_rng(21)
+    xs = rng.standard_normal(3000) * 10.0 ** rng.integers(-42, 38, 3000)
+    ties = [1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 5 * 2 ** -8), 2 ** -130 * 1.5, 2 ** -134, 2 ** -133 * 3]
+    xs = np.concatenate([xs, ties])
+    want = np.array([_rne_exact(float(x), 7, -126) for x in xs])
+    assert np.array_equal(oracle.round_bf16(xs), want)
+    assert oracle.round_bf16(np.array([3.5e38]))[0] == np.inf
+    assert oracle.round_out(np.array([1 + 2 ** -11, 1 + 3 * 2 ** -11]), "f16").tolist() == [1.0, 1 + 2 ** -9]
+
+
+def test_scaled_oracle_pins():
+    """Unit scales and no zero points: the plain exact sum, rounded once. Zero
+    points: brute force over Python integers. Power-of-two scales: exact."""
+    for dt in ("s8", "s4"):
+        M, N, K = 3, 5, 8
+        A, B = si.gen_operands(dt, M, N, K, seed=17)
+        C = (oracle.gemm_s8(A, B) if dt == "s8" else oracle.gemm_s4(A, B)).astype(np.float64)
+        got, exact, D = oracle.gemm_scaled(dt, A, B, "f32")
+        assert D is None and np.array_equal(exact, C) and np.array_equal(got, C.astype(np.float32))
+        za = np.array([3, -2, 0], np.int32)
+        zb = np.array([1, 0, -4, 7, -1], np.int32)
+        a = oracle.s4_unpack(A) if dt == "s4" else A.astype(np.int64)
+        b = oracle.s4_unpack(B) if dt == "s4" else B.astype(np.int64)
+        brute = np.array([[sum((int(a[i, k]) - int(za[i])) * (int(b[j, k]) - int(zb[j])) for k in range(K))
+                           for j in range(N)] for i in range(M)], dtype=np.float64)
+        sa = np.array([0.5, 2.0, 0.25], np.float32)
+        sb = np.array([1.0, 4.0, 0.125, 2.0, 8.0], np.float32)
+        got, exact, _ = oracle.gemm_scaled(dt, A, B, "f32", sa, sb, za, zb)
+        assert np.array_equal(exact, brute * sa[:, None] * sb[None, :])
+    A, B = si.gen_operands("f16", 4, 3, 16, seed=3)
+    C, D = oracle.gemm_f16(A, B)
+    sa = np.array([2.0, 0.5, 1.0, 4.0], np.float32)
+    got, exact, Ds = oracle.gemm_scaled("f16", A, B, "bf16", sa, None)
+    assert np.array_equal(exact, C * sa[:, None]) and np.array_equal(Ds, D * sa[:, None])
+    assert np.array_equal(got, oracle.round_bf16(C * sa[:, None]))
