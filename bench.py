@@ -52,6 +52,13 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 CPU_SAMPLE_ROWS = {"f16": 1024, "s8": 8192, "s4": 8192}
 
 
+def gemm_ops(m: int, n: int, k: int) -> float:
+    """Operations of one GEMM: a multiply and an add per (i, j, k) term, the
+    convention of the paper's throughput figures (its Table II TOPS column is
+    2 * N^3 / duration)."""
+    return 2.0 * m * n * k
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -178,14 +185,14 @@ def main():
     log(f"timed region {wall * 1e3:.1f} ms")
 
     ms_per_step = wall * 1e3 / args.steps
-    total_ops = sum(2.0 * b["n"] ** 3 for b in bufs)
+    total_ops = sum(gemm_ops(b["n"], b["n"], b["n"]) for b in bufs)
     value = total_ops / (ms_per_step * 1e-3) / 1e12
 
     pts = []
     for i, b in enumerate(bufs):
         ms = [evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)]
         mean_ms = float(np.mean(ms))
-        ops = 2.0 * b["n"] ** 3
+        ops = gemm_ops(b["n"], b["n"], b["n"])
         tops = ops / (mean_ms * 1e-3) / 1e12
         pts.append(dict(dtype=b["dt"], n=b["n"], variant=b["vname"], ms=round(mean_ms, 5),
                         ms_min=round(float(np.min(ms)), 5), ms_max=round(float(np.max(ms)), 5),
@@ -210,7 +217,7 @@ def main():
                     frac=round(dom["tops"] / point_peak(dom["dtype"], dom["variant"]), 4),
                     traffic=traffic,
                     algorithmic_bytes=int((2 * IN_BYTES[dom["dtype"]] + 4) * n * n),
-                    algorithmic_ops=int(2 * n ** 3))
+                    algorithmic_ops=int(gemm_ops(n, n, n)))
     for p in pts:
         p.pop("total_ms")
 
@@ -317,7 +324,7 @@ def cpu_baseline(bufs, log):
         else:
             ref, D = oracle.gemm_s4(A, B, rows=rows, threads=threads), None
         dt_s = time.perf_counter() - t0
-        ops = 2.0 * len(rows) * n * n
+        ops = gemm_ops(len(rows), n, n)
         total_ops += ops
         total_s += dt_s
         got = b["C"][torch.from_numpy(rows.astype(np.int64)).to(b["C"].device)].cpu().numpy()

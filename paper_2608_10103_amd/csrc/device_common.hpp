@@ -19,6 +19,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace mpg {
 
 enum Dtype : int { F16 = 0, S8 = 1, S4 = 2 };
@@ -179,6 +182,20 @@ __device__ __forceinline__ void epi_store_one(const EpiParams &e, void *C, long 
     store_out(e, C, i * N + j, epi_value<DT>(e, x, i, sb, zb, cs));
 }
 
+// Calls f(integral_constant<int, I>) for I = 0 .. N-1, unrolled by
+// construction. The epilogue indexes the accumulator arrays only through
+// such compile-time indices: a loop the unroller declines (it does for the
+// scaled path of a 128 x 128 wave tile) would index them at run time and
+// move every accumulator to scratch memory.
+template <class F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // A wave's MS x MS blocks (FM x FN of them): block (i, j) value v of lane
 // group h sits at row row0 + i MS + acc_row(h, v), column col0 + j MS (col0
 // includes the lane's column). conv maps an accumulator element to the raw
@@ -189,39 +206,38 @@ __device__ __forceinline__ void epi_store_tile(const EpiParams &e, void *C, cons
     typedef typename Acc<DT, MS>::out out_t;
     if (e.out == OUT_PLAIN) {
         out_t *Co = reinterpret_cast<out_t *>(C);
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-#pragma unroll
-                for (int v = 0; v < NV; ++v) {
+        static_for<FM>([&](auto i) __attribute__((always_inline)) {
+            static_for<FN>([&](auto j) __attribute__((always_inline)) {
+                static_for<NV>([&](auto v) __attribute__((always_inline)) {
                     const long row = row0 + i * MS + acc_row<MS>(h, v), col = col0 + j * MS;
-                    if (row < M && col < N) Co[row * N + col] = conv(acc[i][j][v]);
-                }
+                    if (row < M && col < N) Co[row * N + col] = conv(acc[i][j][v.value]);
+                });
+            });
+        });
         return;
     }
     float sb[FN];
     long long zb[FN], cs[FN];
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
+    static_for<FN>([&](auto j) __attribute__((always_inline)) {
         const long col = col0 + j * MS;
         const bool ok = col < N;
         sb[j] = (e.scale_b && ok) ? e.scale_b[col] : 1.0f;
         zb[j] = (e.zero_b && ok) ? e.zero_b[col] : 0;
         cs[j] = (e.zero_a && ok) ? e.sum_b[col] : 0;
-    }
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int v = 0; v < NV; ++v) {
+    });
+    static_for<FM>([&](auto i) __attribute__((always_inline)) {
+        static_for<NV>([&](auto v) __attribute__((always_inline)) {
             const long row = row0 + i * MS + acc_row<MS>(h, v);
-            if (row >= M) continue;
-#pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const long col = col0 + j * MS;
-                if (col < N) store_out(e, C, row * N + col, epi_value<DT>(e, conv(acc[i][j][v]), row, sb[j], zb[j], cs[j]));
+            if (row < M) {
+                static_for<FN>([&](auto j) __attribute__((always_inline)) {
+                    const long col = col0 + j * MS;
+                    if (col < N)
+                        store_out(e, C, row * N + col,
+                                  epi_value<DT>(e, conv(acc[i][j][v.value]), row, sb[j], zb[j], cs[j]));
+                });
             }
-        }
+        });
+    });
 }
 
 // Accumulator element -> raw sum.

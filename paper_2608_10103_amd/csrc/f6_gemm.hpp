@@ -126,7 +126,7 @@ struct F6Prep {
 // and runs past the data are written as zero codes.
 constexpr int F6_PREP_ROWS = 32, F6_PREP_RUNS = 32, F6_PREP_PITCH = 33;
 
-__global__ __launch_bounds__(256) void s4_to_e3m2(F6Prep a, F6Prep b) {
+inline __global__ __launch_bounds__(256) void s4_to_e3m2(F6Prep a, F6Prep b) {
     __shared__ __attribute__((aligned(16))) uint8_t lp[F6_PREP_RUNS * F6_PREP_PITCH * 16];
     __shared__ __attribute__((aligned(16))) uint8_t lq[F6_PREP_RUNS * F6_PREP_PITCH * 8];
     const F6Prep &o = blockIdx.z ? b : a;

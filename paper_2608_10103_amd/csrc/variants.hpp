@@ -1,0 +1,161 @@
+// variants.hpp - the kernel variant table: tile configurations, the record
+// the host code launches from, and the list of variants every precision
+// carries. Each precision's table is built in its own translation unit
+// (variants_f16.hip, variants_s8.hip, variants_s4.hip) so the kernels of the
+// three precisions compile in parallel; mpgemm.hip selects and launches.
+#pragma once
+
+#include <stdint.h>
+
+#include "generic_gemm.hpp"
+#include "tiled_gemm.hpp"
+#include "f6_gemm.hpp"
+
+// Tile configurations (kernel template arguments need external linkage).
+namespace mpg {
+//                BM   BN  WGM WGN BKB STG GROUP_M
+typedef TileCfg<256, 256, 2, 2, 128, 2, 4> T256x256_w4_s2;
+typedef TileCfg<256, 256, 2, 4, 128, 2, 4> T256x256_w8_s2;
+typedef TileCfg<256, 256, 4, 2, 128, 2, 4> T256x256_w8t_s2;
+typedef TileCfg<256, 256, 4, 4, 128, 2, 4> T256x256_w16_s2;
+typedef TileCfg<256, 256, 4, 2, 64, 4, 4> T256x256_w8t_k64_s4;
+typedef TileCfg<256, 256, 4, 4, 64, 4, 4> T256x256_w16_k64_s4;
+typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4b;
+typedef TileCfg<128, 128, 2, 2, 64, 4, 4> T128x128_w4_k64_s4;
+typedef TileCfg<256, 256, 2, 2, 64, 2, 4> T256x256_w4_k64_s2;
+typedef TileCfg<256, 256, 4, 2, 64, 2, 4> T256x256_w8t_k64_s2;
+typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_k128_s2;
+typedef TileCfg<256, 256, 2, 4, 64, 2, 4> T256x256_w8_k64_s2;
+typedef TileCfg<128, 128, 2, 2, 128, 4, 4, 16> T128x128_w4_s4_m16;
+typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4;
+typedef TileCfg<256, 128, 2, 2, 128, 3, 4> T256x128_w4_s3;
+typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
+typedef TileCfg<128, 128, 2, 2, 128, 4, 4> T128x128_w4_s4;
+typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
+typedef TileCfg<256, 256, 2, 4, 64, 4, 4> T256x256_w8_k64_s4;
+typedef TileCfg<256, 256, 2, 4, 64, 3, 4> T256x256_w8_k64_s3;
+
+//             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
+typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
+typedef F6Cfg<256, 256, 2, 4, 4, 2, 4> F6_256x256_w8_s2;
+typedef F6Cfg<256, 256, 2, 2, 4, 3, 4> F6_256x256_w4_s3;
+typedef F6Cfg<256, 256, 4, 2, 4, 3, 4> F6_256x256_w8t_s3;
+typedef F6Cfg<256, 128, 2, 2, 4, 4, 4> F6_256x128_w4_s4;
+typedef F6Cfg<128, 128, 2, 2, 4, 4, 4> F6_128x128_w4_s4;
+typedef F6Cfg<128, 128, 2, 2, 4, 6, 4> F6_128x128_w4_s6;
+typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
+
+}  // namespace mpg
+
+namespace mpg {
+
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2 };
+
+struct Variant {
+    const char *name;
+    int kind;
+    int bm, bn, bkb;  // tile; bkb: bytes per row per K-slice (TILED), runs per stage (FP6)
+    int threads;
+    const void *fn;
+    bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
+};
+
+typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int,
+                          EpiParams);
+typedef void (*splitk_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int, int,
+                          int *, uint32_t *, EpiParams);
+typedef void (*generic_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int,
+                           EpiParams);
+
+template <int DT, class T>
+Variant tiled(const char *name) {
+    kernel_fn f = &tiled_gemm<DT, T>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
+template <int DT, class T, bool SPREAD = false>
+Variant pipelined(const char *name) {
+    splitk_fn f = &tiled_gemm_pf<DT, T, SPREAD>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   true};
+}
+
+template <int DT, class T, int NSETS>
+Variant staged(const char *name) {
+    kernel_fn f = &tiled_gemm_rs<DT, T, NSETS>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
+template <int DT, class T, int LEFT>
+Variant pingpong(const char *name) {
+    kernel_fn f = &tiled_gemm_pp<DT, T, LEFT>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
+template <class T>
+Variant fp6(const char *name) {
+    typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
+                          int32_t *, int, int, int, int, int, int, int, EpiParams);
+    f6_fn f = &f6_gemm<T>;
+    return Variant{name, FP6, T::BM, T::BN, T::J, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
+template <int DT>
+Variant generic(const char *name) {
+    generic_fn f = &generic_gemm<DT>;
+    return Variant{name, GENERIC, 32, 32, 0, 64, reinterpret_cast<const void *>(f), false};
+}
+
+#define VARIANT_LIST(DT)                                                   \
+    generic<DT>("generic_32x32"),                                          \
+     tiled<DT, T256x256_w4_s2>("tile256x256_w2x2_k128_s2"),                \
+     tiled<DT, T256x256_w8_s2>("tile256x256_w2x4_k128_s2"),                \
+     tiled<DT, T256x256_w4_k64_s4>("tile256x256_w2x2_k64_s4"),             \
+     tiled<DT, T256x128_w4_s3>("tile256x128_w2x2_k128_s3"),                \
+     tiled<DT, T128x128_w4_s2>("tile128x128_w2x2_k128_s2"),                \
+     tiled<DT, T128x128_w4_s4>("tile128x128_w2x2_k128_s4"),                \
+     tiled<DT, T64x64_w1_s4>("tile64x64_w1x1_k128_s4"),                    \
+     pipelined<DT, T256x256_w4_s2>("pipe256x256_w2x2_k128_s2"),            \
+     pipelined<DT, T256x256_w8_s2>("pipe256x256_w2x4_k128_s2"),            \
+     pipelined<DT, T256x256_w4_k64_s4>("pipe256x256_w2x2_k64_s4"),         \
+     pipelined<DT, T256x128_w4_s3>("pipe256x128_w2x2_k128_s3"),            \
+     pipelined<DT, T128x128_w4_s4>("pipe128x128_w2x2_k128_s4"),            \
+     pipelined<DT, T64x64_w1_s4>("pipe64x64_w1x1_k128_s4"),                \
+     pipelined<DT, T256x256_w8t_s2>("pipe256x256_w4x2_k128_s2"),           \
+     pipelined<DT, T256x256_w16_s2>("pipe256x256_w4x4_k128_s2"),           \
+     pipelined<DT, T256x256_w8t_k64_s4, true>("spread256x256_w4x2_k64_s4"), \
+     pipelined<DT, T256x256_w8t_s2, true>("spread256x256_w4x2_k128_s2"),   \
+     pipelined<DT, T256x256_w16_k64_s4, true>("spread256x256_w4x4_k64_s4"), \
+     pipelined<DT, T256x256_w4_k64_s4b, true>("spread256x256_w2x2_k64_s4"), \
+     pipelined<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4"),    \
+     pipelined<DT, T128x128_w4_k64_s4, true>("spread128x128_w2x2_k64_s4"), \
+     staged<DT, T256x256_w4_s2, 2>("staged256x256_w2x2_k128_n2"),          \
+     staged<DT, T256x256_w4_s2, 1>("staged256x256_w2x2_k128_n1"),          \
+     staged<DT, T256x256_w8t_s2, 1>("staged256x256_w4x2_k128_n1"),         \
+     staged<DT, T256x256_w8_s2, 1>("staged256x256_w2x4_k128_n1"),          \
+     staged<DT, T256x256_w4_k64_s2, 2>("staged256x256_w2x2_k64_n2"),       \
+     staged<DT, T256x256_w8t_k64_s2, 2>("staged256x256_w4x2_k64_n2"),      \
+     staged<DT, T128x128_w4_k128_s2, 2>("staged128x128_w2x2_k128_n2"),     \
+     pingpong<DT, T256x256_w8_s2, 4>("pingpong256x256_k128_c4"),          \
+     pingpong<DT, T256x256_w8_s2, 2>("pingpong256x256_k128_c2"),          \
+     pingpong<DT, T256x256_w8_s2, 6>("pingpong256x256_k128_c6"),          \
+     pingpong<DT, T256x256_w8_k64_s2, 4>("pingpong256x256_k64_c4"),       \
+     pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16"), \
+     pipelined<DT, T256x256_w8_k64_s4>("pipe256x256_w2x4_k64_s4"),          \
+     pipelined<DT, T256x256_w8_k64_s3>("pipe256x256_w2x4_k64_s3")
+
+// Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
+// them (variants_s4.hip); each table checks its size against these.
+constexpr int kNumCommon = 36;
+constexpr int kNumFp6 = 8;
+constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
+
+extern const Variant kF16[];
+extern const Variant kS8[];
+extern const Variant kS4[];
+
+}  // namespace mpg
