@@ -105,13 +105,17 @@ __device__ __forceinline__ int s4_nibble(uint32_t byte, int which) {
 }
 
 // LDS swizzle: in a tile of rows of CH 16-byte chunks, chunk c of row q is
-// stored at slot c ^ swz(q). Chosen so that the 16-byte reads of 32
-// consecutive rows at one chunk index (what one MFMA operand fetch does) hit
-// distinct bank groups both in 8-lane (128-byte) and 16-lane (256-byte)
-// service groups.
+// stored at slot c ^ swz(q). An MFMA operand fetch reads one chunk index of 32
+// consecutive rows (16 bytes per lane). 128-byte rows: rows 8 apart get
+// different slots, which keeps every 8 consecutive lanes on distinct 16-byte
+// bank groups (no bank conflicts counted by SQ_LDS_BANK_CONFLICT). 64-byte
+// rows: the swizzle was chosen by measurement on MI355X among the functions
+// ((q >> a) ^ (q >> b)) & 3: this one reads at the conflict-free rate of the
+// 128-byte layout, while ((q >> 1) ^ (q >> 3)) & 3, conflict-free for 16
+// consecutive lanes on paper, reads 1.75x slower.
 template <int CH> __host__ __device__ constexpr int swz(int q) {
     if constexpr (CH == 8) return (q ^ (q >> 3)) & 7;
-    else if constexpr (CH == 4) return ((q >> 1) ^ (q >> 3)) & 3;
+    else if constexpr (CH == 4) return ((q >> 3) ^ (q >> 4)) & 3;
     else return 0;
 }
 

@@ -10,6 +10,7 @@
 #include "generic_gemm.hpp"
 #include "tiled_gemm.hpp"
 #include "f6_gemm.hpp"
+#include "deep_gemm.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -34,6 +35,7 @@ typedef TileCfg<128, 128, 2, 2, 128, 4, 4> T128x128_w4_s4;
 typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 4, 4> T256x256_w8_k64_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 3, 4> T256x256_w8_k64_s3;
+typedef TileCfg<256, 256, 2, 2, 64, 5, 4> T256x256_w4_k64_s5;
 
 //             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
 typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
@@ -95,6 +97,13 @@ Variant pingpong(const char *name) {
                    false};
 }
 
+template <int DT, class T>
+Variant deep(const char *name) {
+    kernel_fn f = &tiled_gemm_deep<DT, T>;
+    return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
 template <class T>
 Variant fp6(const char *name) {
     typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
@@ -146,11 +155,13 @@ Variant generic(const char *name) {
      pingpong<DT, T256x256_w8_k64_s2, 4>("pingpong256x256_k64_c4"),       \
      pipelined<DT, T128x128_w4_s4_m16, true>("spread128x128_w2x2_k128_s4_m16"), \
      pipelined<DT, T256x256_w8_k64_s4>("pipe256x256_w2x4_k64_s4"),          \
-     pipelined<DT, T256x256_w8_k64_s3>("pipe256x256_w2x4_k64_s3")
+     pipelined<DT, T256x256_w8_k64_s3>("pipe256x256_w2x4_k64_s3"),          \
+     deep<DT, T256x256_w4_k64_s4>("deep256x256_w2x2_k64_s4"),             \
+     deep<DT, T256x256_w4_k64_s5>("deep256x256_w2x2_k64_s5")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 36;
+constexpr int kNumCommon = 38;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

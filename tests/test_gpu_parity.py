@@ -117,6 +117,8 @@ def _variant_shapes(dtype, v):
     kb = int(name.split("_k")[1].split("_")[0])
     elems_per_kb = {"f16": kb // 2, "s8": kb, "s4": 2 * kb}[dtype]
     return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb),
+            # more K-slices than a 4- or 5-deep ring holds, not a multiple of 3
+            (bm, 2 * bn, 7 * elems_per_kb),
             # ragged M and N: predicated edge tiles
             (2 * bm + 17, bn + 5, 3 * elems_per_kb), (1, bn - 1, elems_per_kb), (bm + 31, 1, 2 * elems_per_kb)]
 
