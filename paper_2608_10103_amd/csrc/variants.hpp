@@ -11,6 +11,7 @@
 #include "tiled_gemm.hpp"
 #include "f6_gemm.hpp"
 #include "deep_gemm.hpp"
+#include "skinny_gemm.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -51,12 +52,14 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3 };
 
 struct Variant {
     const char *name;
     int kind;
-    int bm, bn, bkb;  // tile; bkb: bytes per row per K-slice (TILED), runs per stage (FP6)
+    int bm, bn, bkb;  // tile; bkb: bytes per row per K-slice (TILED), runs per stage (FP6);
+                      // SKINNY: bm = most rows of the small operand, bn = rows of the
+                      // large one per workgroup, bkb = bytes per K-step
     int threads;
     const void *fn;
     bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
@@ -101,6 +104,15 @@ template <int DT, class T>
 Variant deep(const char *name) {
     kernel_fn f = &tiled_gemm_deep<DT, T>;
     return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
+}
+
+template <int DT, int MB, int NB>
+Variant skinny(const char *name) {
+    typedef void (*skinny_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int,
+                              EpiParams);
+    skinny_fn f = &skinny_gemm<DT, MB, NB>;
+    return Variant{name, SKINNY, 16 * MB, 16 * NB, 64, 64 * SKINNY_WAVES, reinterpret_cast<const void *>(f),
                    false};
 }
 
@@ -157,11 +169,15 @@ Variant generic(const char *name) {
      pipelined<DT, T256x256_w8_k64_s4>("pipe256x256_w2x4_k64_s4"),          \
      pipelined<DT, T256x256_w8_k64_s3>("pipe256x256_w2x4_k64_s3"),          \
      deep<DT, T256x256_w4_k64_s4>("deep256x256_w2x2_k64_s4"),             \
-     deep<DT, T256x256_w4_k64_s5>("deep256x256_w2x2_k64_s5")
+     deep<DT, T256x256_w4_k64_s5>("deep256x256_w2x2_k64_s5"),             \
+     skinny<DT, 1, 1>("skinny16x16_k64"),                                 \
+     skinny<DT, 1, 2>("skinny16x32_k64"),                                 \
+     skinny<DT, 2, 1>("skinny32x16_k64"),                                 \
+     skinny<DT, 2, 2>("skinny32x32_k64")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 38;
+constexpr int kNumCommon = 42;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -34,7 +34,7 @@ def test_variant_table():
         n = mp.num_variants(dt)
         assert n >= 2
         assert mp.variant_name(dt, 0).startswith("generic")
-        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep") + (("fp6pipe",) if dt == "s4" else ())
+        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny") + (("fp6pipe",) if dt == "s4" else ())
         assert all(mp.variant_name(dt, v).startswith(prefixes) for v in range(1, n))
         assert mp.variant_name(dt, n) == ""
     assert mp.lib().mpgemm_num_variants(7) == -1
@@ -179,20 +179,47 @@ def test_fp6_variants_bound_k():
         assert not any(mp.variant_name(dt, v).startswith("fp6") for v in range(mp.num_variants(dt)))
 
 
+def test_skinny_selection():
+    """At most 16 rows (FP16) or 32 rows (integers) on one side and at least
+    1024 on the other: the streaming kernel, 32 large-side rows per workgroup
+    when a wave has at most 8 K-steps of 64 bytes or the small side needs two
+    16-row blocks; never split."""
+    name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
+    for dt in ("f16", "s8", "s4"):
+        for M in (1, 7, 16):
+            assert name(dt, M, 8192, 8192).startswith("skinny16x"), (dt, M)
+            assert name(dt, 8192, M, 8192).startswith("skinny16x"), (dt, M)  # small N: operands swapped
+            v = mp.select_variant(dt, M, 8192, 8192)
+            assert mp.select_splits(dt, v, M, 8192, 8192) == 1
+        assert not name(dt, 16, 1000, 8192).startswith("skinny")  # large side too small
+        assert not name(dt, 16, 8192, 8192, a_ptr=(1 << 20) + 4).startswith("skinny")  # unaligned A
+    assert name("f16", 16, 8192, 8192) == "skinny16x16_k64"    # 32 K-steps per wave
+    assert name("f16", 32, 8192, 8192).startswith("spread128")  # FP16 beyond 16 rows: tiled
+    assert name("s8", 16, 8192, 8192) == "skinny16x16_k64"     # 16 K-steps per wave
+    assert name("s8", 16, 14336, 4096) == "skinny16x32_k64"    # 8 K-steps per wave
+    assert name("s8", 32, 8192, 8192) == "skinny32x32_k64"
+    assert name("s4", 16, 8192, 8192) == "skinny16x32_k64"     # 8 K-steps per wave
+    assert name("s4", 16, 4096, 14336) == "skinny16x16_k64"    # 14 K-steps per wave
+    assert name("s4", 24, 8192, 8192) == "skinny32x32_k64"
+    assert not name("s8", 33, 8192, 8192).startswith("skinny")
+    assert not name("s8", 16, 8192, 8160).startswith("skinny")  # K off the 64-byte step
+
+
 def test_split_k_selection():
-    """Only skinny problems (M or N <= 128) are split; FP16 up to 4 K-ranges,
-    integers up to 2; square sweep sizes never."""
+    """Only problems with M or N <= 128 that the streaming kernel does not
+    take are split; FP16 up to 4 K-ranges, integers up to 2; square sweep
+    sizes never."""
     for dt, most in (("f16", 4), ("s8", 2), ("s4", 2)):
         for n in (512, 1024, 2048, 4096, 8192):
             v = mp.select_variant(dt, n, n, n)
             assert mp.select_splits(dt, v, n, n, n) == 1
-        for M in (1, 16, 128):
+        for M in (64, 128) + ((32,) if dt == "f16" else ()):
             v = mp.select_variant(dt, M, 8192, 8192)
             assert mp.variant_name(dt, v).startswith("spread128")
             assert mp.select_splits(dt, v, M, 8192, 8192) == most
             assert mp.select_splits(dt, v, 8192, M, 8192) == most
-        v = mp.select_variant(dt, 16, 8192, 1024)
-        assert mp.select_splits(dt, v, 16, 8192, 1024) <= most  # every range keeps >= 8 slices
+        v = mp.select_variant(dt, 64, 8192, 1024)
+        assert mp.select_splits(dt, v, 64, 8192, 1024) <= most  # every range keeps >= 8 slices
     assert mp.select_splits("s8", 0, 16, 8192, 8192) == 1  # the bounds-checked kernel never splits
     L = mp.lib()
     assert L.mpgemm_select_splits(7, 1, 16, 16, 16) == -1

@@ -108,6 +108,14 @@ def _variant_shapes(dtype, v):
     name = mp.variant_name(dtype, v)
     if name.startswith("generic"):
         return [(97, 65, 130), (33, 31, 66)]
+    if name.startswith("skinny"):
+        # at most `rows` rows on the small side (either side); whole 64-byte
+        # K-steps split over 8 waves: fewer steps than waves, step counts off
+        # the 4-step prefetch group, long K; ragged large side
+        rows, per_wg = (int(x) for x in re.match(r"skinny(\d+)x(\d+)_", name).groups())
+        e = {"f16": 32, "s8": 64, "s4": 128}[dtype]  # elements per 64-byte step
+        return [(rows, 3 * per_wg + 5, 9 * e), (1, per_wg, e), (rows - 3, 700, 40 * e),
+                (2 * per_wg + 7, rows, 17 * e), (300, 1, 5 * e), (rows // 2 + 1, 64, 3 * e)]
     bm, bn = (int(x) for x in re.match(r"(?:fp6)?[a-z]+(\d+)x(\d+)_", name).groups())
     if name.startswith("fp6"):
         # INT4 on the FP6 cores: any even K (zero-padded to whole stages)
