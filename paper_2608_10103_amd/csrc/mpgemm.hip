@@ -441,6 +441,26 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
 
 extern "C" {
 
+hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                          hipStream_t stream) {
+    if (dtype != F16 && dtype != S8) return hipErrorInvalidValue;
+    // the size, pointer and overlap checks of the plain entry points (B
+    // occupies K * N elements either way)
+    if (!valid_args(dtype, M, N, K, A, B, C)) return hipErrorInvalidValue;
+    if (M == 0 || N == 0) return hipSuccess;
+    if (K == 0) return run(dtype, -1, -1, M, N, K, A, B, C, stream);  // zero fill
+    typedef TileCfg<256, 256, 2, 4, 128, 2, 4> T;
+    const long kb = row_bytes(dtype, K);
+    if (N % T::BN || kb % T::BKB || !aligned(A, 16) || !aligned(B, 16)) return hipErrorInvalidValue;
+    if (kb > INT_MAX || (long)K * N > (long)INT_MAX * 16) return hipErrorInvalidValue;
+    const uint8_t *a = static_cast<const uint8_t *>(A), *b = static_cast<const uint8_t *>(B);
+    int kbi = (int)kb, tiles_m = (M + T::BM - 1) / T::BM, tiles_n = N / T::BN;
+    EpiParams epi = plain_epilogue(K);
+    void *args[] = {&a, &b, &C, &M, &N, &kbi, &tiles_m, &tiles_n, &epi};
+    return hipLaunchKernel(tposeb_kernel(dtype), dim3(tiles_m * tiles_n), dim3(T::NTHREADS), args, 0,
+                           stream);
+}
+
 hipError_t gemm_f16_f32(int M, int N, int K, const void *A, const void *B, float *C,
                         hipStream_t stream) {
     return run(F16, -1, -1, M, N, K, A, B, C, stream);

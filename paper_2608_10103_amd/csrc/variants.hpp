@@ -181,6 +181,9 @@ constexpr int kNumCommon = 42;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 
+// Kernel of the transposed-B entry point (tposeb.hip): F16 or S8, else null.
+const void *tposeb_kernel(int dtype);
+
 extern const Variant kF16[];
 extern const Variant kS8[];
 extern const Variant kS4[];

@@ -66,6 +66,7 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_run_variant_scaled.argtypes = [I, I, I, I, I, I, P, P, P, P, P]
     L.mpgemm_run_variant_scaled.restype = I
     L.mpgemm_s4_run_to_fp6.argtypes = [P, P]
+    L.mpgemm_gemm_bt.argtypes = [I, I, I, I, P, P, P, P]
     L.mpgemm_s4_run_to_fp6.restype = None
     _lib = L
     return L
@@ -74,7 +75,7 @@ def lib() -> ctypes.CDLL:
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
                     "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
                     "mpgemm_run_variant", "mpgemm_select_splits", "mpgemm_run_variant_splits",
-                    "gemm_scaled", "mpgemm_run_variant_scaled", "mpgemm_s4_run_to_fp6")
+                    "gemm_scaled", "mpgemm_run_variant_scaled", "mpgemm_s4_run_to_fp6", "mpgemm_gemm_bt")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -151,6 +152,33 @@ def gemm_s4_s32(A, B, C=None, stream=None, variant=None, splits=None):
 
 
 GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
+
+
+def gemm_bt(dtype: str, A, B_kn, C=None, stream=None):
+    """C = A * B with B given K x N row-major (N-contiguous), FP16 or INT8
+    (mpgemm_gemm_bt): A (M, K), B_kn (K, N) of the dtype's input type."""
+    if dtype not in ("f16", "s8"):
+        raise ValueError("transposed B: f16 or s8")
+    want = _IN_DTYPE[dtype]
+    for name, t in (("A", A), ("B", B_kn)):
+        if not isinstance(t, torch.Tensor) or t.dtype != want or t.dim() != 2:
+            raise TypeError(f"{name} must be a 2-D {want} tensor")
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if A.device != B_kn.device:
+        raise ValueError("A and B must be on the same device")
+    M, K = A.shape
+    KB, N = B_kn.shape
+    if K != KB:
+        raise ValueError(f"K mismatch: A has {K}, B has {KB} rows")
+    C = _out(dtype, M, N, A, C)
+    s = _stream_ptr(stream, A.device)
+    with torch.cuda.device(A.device):
+        code = lib().mpgemm_gemm_bt(DTYPE_CODE[dtype], M, N, K, A.data_ptr(), B_kn.data_ptr(),
+                                    C.data_ptr(), s)
+    if code != 0:
+        raise HipError(code, f"transposed-B {dtype} GEMM {M}x{N}x{K}")
+    return C
 
 
 class Epilogue(ctypes.Structure):

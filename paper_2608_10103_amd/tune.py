@@ -44,6 +44,9 @@ def main(argv=None) -> int:
     ap.add_argument("--variants", default="", help="comma-separated names or substrings")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--json", default="", help="write the results here")
+    ap.add_argument("--transposed-b", action="store_true",
+                    help="also time mpgemm_gemm_bt (B stored K x N row-major) on the same operands "
+                         "(FP16, INT8)")
     args = ap.parse_args(argv)
     want = [w for w in args.variants.split(",") if w]
     stream = torch.cuda.Stream()
@@ -75,6 +78,10 @@ def main(argv=None) -> int:
                     except mp.HipError:
                         continue
                     runs.append((v, sp, f"{name} splits {sp}"))
+            Bt = None
+            if args.transposed_b and dt in ("f16", "s8"):
+                Bt = Bd.t().contiguous()  # the same B, K x N row-major
+                runs.append(("bt", None, "transposed B (mpgemm_gemm_bt)"))
             if not runs:
                 continue
             out_dt = torch.float32 if dt == "f16" else torch.int32
@@ -84,7 +91,10 @@ def main(argv=None) -> int:
 
             def call(i):
                 v, sp, _ = runs[i]
-                mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp)
+                if v == "bt":
+                    mp.gemm_bt(dt, Ad, Bt, C=Cs[i], stream=stream)
+                else:
+                    mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp)
 
             with torch.cuda.stream(stream):
                 for i in range(len(runs)):
@@ -105,7 +115,7 @@ def main(argv=None) -> int:
             for i, (v, sp, label) in enumerate(runs):
                 ms = float(np.median(times[i]))
                 tops = 2 * M * N * K / (ms * 1e-3) / 1e12
-                name = mp.variant_name(dt, v)
+                name = "transposed_b" if v == "bt" else mp.variant_name(dt, v)
                 peak = PEAK_FP6 if name.startswith("fp6") else PEAK[dt]
                 if i == 0:
                     same = "ref"
@@ -114,12 +124,13 @@ def main(argv=None) -> int:
                 else:
                     same = "identical" if torch.equal(Cs[i], ref) else "DIFFERENT"
                 spread = 100 * (max(times[i]) - min(times[i])) / ms
-                print(f"{dt} {M}x{N}x{K} v{v:2d} {label:44s} {ms * 1e3:9.1f} us {tops:8.1f} T/s "
+                vtag = "bt" if v == "bt" else f"{v:2d}"
+                print(f"{dt} {M}x{N}x{K} v{vtag} {label:44s} {ms * 1e3:9.1f} us {tops:8.1f} T/s "
                       f"{100 * tops / peak:5.1f}% of peak  rel {base / ms:5.3f}  spread {spread:4.1f}%  {same}",
                       flush=True)
                 res.append(dict(dtype=dt, M=M, N=N, K=K, variant=v, name=name, splits=sp, us=ms * 1e3,
                                 tops=tops, frac_peak=tops / peak, rel=base / ms, check=same))
-            del Cs, Ad, Bd
+            del Cs, Ad, Bd, Bt
             torch.cuda.empty_cache()
     if args.json:
         with open(args.json, "w") as f:

@@ -565,3 +565,73 @@ def test_scaled_argument_errors():
     assert call(1, t, E(None, None, None, None, 2), c.data_ptr() + 1) == INVALID  # FP16 output: 2-byte C
     assert call(1, t, E(s.data_ptr(), s.data_ptr(), z.data_ptr(), z.data_ptr(), 3)) == 0
     torch.cuda.synchronize()
+
+
+# ------------------------------------------------- B stored K x N row-major
+
+
+def _gpu_gemm_bt(dtype, A, B_kn):
+    C = mp.gemm_bt(dtype, dev(A), dev(B_kn))
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", ["f16", "s8"])
+def test_transposed_b_parity(dtype):
+    """mpgemm_gemm_bt (B(k, j) at k * N + j) against the oracle on the same
+    B transposed on the host to the oracle's N rows of K: several tiles and
+    K-slices, the 2-slice ring's steady state and tail, ragged M."""
+    kslice = 64 if dtype == "f16" else 128
+    for (M, N, K) in [(256, 256, kslice), (512, 768, 5 * kslice), (300, 256, 3 * kslice),
+                      (1, 512, 2 * kslice), (777, 1024, 7 * kslice)]:
+        A, B = si.gen_operands(dtype, M, N, K, seed=900 + M + N + K)  # B: N rows of K
+        B_kn = np.ascontiguousarray(B.T)  # the same matrix, K x N row-major
+        C = _gpu_gemm_bt(dtype, A, B_kn)
+        assert_parity(dtype, C, *oracle_gemm(dtype, A, B), f"{dtype} transposed B {M}x{N}x{K}")
+    _log(f"{dtype} transposed B: ok")
+
+
+@pytest.mark.parametrize("dtype", ["f16", "s8"])
+def test_transposed_b_full_size_sampled_rows(dtype):
+    """N = 8192 (the measured size): 40 sampled rows against the oracle."""
+    n = 8192
+    A, B = si.gen_operands(dtype, n, n, n, seed=31)
+    C = _gpu_gemm_bt(dtype, A, np.ascontiguousarray(B.T))
+    rows = np.random.default_rng(31).choice(n, size=38, replace=False).tolist() + [0, n - 1]
+    C_ref, D = oracle_gemm(dtype, A, B, rows=rows)
+    assert_parity(dtype, C[rows], C_ref, D, f"{dtype} transposed B {n}^3 sampled rows")
+
+
+def test_transposed_b_closed_forms():
+    """Identity as B: C = A exactly (integer-valued FP16, INT8); all-ones:
+    C = K."""
+    for dtype, K in (("f16", 256), ("s8", 256)):
+        M = N = 256
+        vals = np.random.default_rng(5).integers(-8, 9, size=(M, K))
+        A = vals.astype(np.float16) if dtype == "f16" else vals.astype(np.int8)
+        eye = np.eye(K, N, dtype=A.dtype)
+        C = _gpu_gemm_bt(dtype, A, eye)
+        want = A[:, :N].astype(np.float32) if dtype == "f16" else A[:, :N].astype(np.int32)
+        assert np.array_equal(C, want), dtype
+        ones_a = np.ones((M, K), dtype=A.dtype)
+        ones_b = np.ones((K, N), dtype=A.dtype)
+        assert np.all(_gpu_gemm_bt(dtype, ones_a, ones_b) == K), dtype
+
+
+def test_transposed_b_argument_errors():
+    A, B = si.gen_operands("f16", 256, 256, 64, seed=1)
+    Ad, Bd = dev(A), dev(np.ascontiguousarray(B.T))
+    for bad in [lambda: mp.gemm_bt("f16", Ad[:, :32].contiguous(), Bd[:32].contiguous()),  # K off the slice
+                lambda: mp.gemm_bt("f16", Ad, Bd[:, :200].contiguous())]:                    # N off the tile
+        with pytest.raises(mp.HipError):
+            bad()
+    with pytest.raises(ValueError):
+        mp.gemm_bt("s4", Ad, Bd)
+    L = mp.lib()
+    assert L.mpgemm_gemm_bt(2, 256, 256, 64, Ad.data_ptr(), Bd.data_ptr(), Ad.data_ptr(), None) != 0
+    assert L.mpgemm_gemm_bt(0, 256, 256, 64, Ad.data_ptr() + 2, Bd.data_ptr(), None, None) != 0
+    # K = 0: zero fill
+    C = torch.full((4, 256), 7.0, dtype=torch.float32, device="cuda")
+    assert L.mpgemm_gemm_bt(0, 4, 256, 0, Ad.data_ptr(), Bd.data_ptr(), C.data_ptr(), None) == 0
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(C).item() == 0
