@@ -63,14 +63,29 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_hash() -> str:
-    """Hash of the HIP sources, to tell whether stored counters still apply."""
-    h = hashlib.sha256()
+# Sources that define each kernel family (by variant-name prefix), besides
+# device_common.hpp and the build flags: stored counters stay valid while
+# these are unchanged.
+KERNEL_SOURCES = {"generic": ["generic_gemm.hpp"], "tile": ["tiled_gemm.hpp"], "pipe": ["tiled_gemm.hpp"],
+                  "spread": ["tiled_gemm.hpp"], "staged": ["tiled_gemm.hpp"],
+                  "pingpong": ["tiled_gemm.hpp"], "fp6pipe": ["tiled_gemm.hpp", "f6_gemm.hpp"],
+                  "deep": ["tiled_gemm.hpp", "deep_gemm.hpp"], "skinny": ["skinny_gemm.hpp"]}
+
+
+def kernel_source_hash(variant_name: str) -> str:
+    """Hash of the sources that define a variant's kernel (its family's
+    headers, device_common.hpp and the build flags), to tell whether stored
+    counters still apply to it."""
+    fam = next((k for k in sorted(KERNEL_SOURCES, key=len, reverse=True) if variant_name.startswith(k)), None)
+    if fam is None:
+        raise ValueError(f"unknown kernel family of {variant_name}")
     csrc = os.path.join(ROOT, "paper_2608_10103_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".hpp")):
-            h.update(f.encode())
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    files = [os.path.join(csrc, f) for f in ["device_common.hpp"] + KERNEL_SOURCES[fam]]
+    files.append(os.path.join(ROOT, "paper_2608_10103_amd", "build.py"))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -207,7 +222,7 @@ def main():
             tr = json.load(open(TRAFFIC_FILE))
             key = f'{dom["dtype"]}:{n}:{dom["variant"]}'
             ent = tr.get("points", {}).get(key)
-            if ent and tr.get("kernel_source_hash") == kernel_source_hash():
+            if ent and ent.get("kernel_source_hash") == kernel_source_hash(dom["variant"]):
                 traffic = ent["hbm_bytes_per_launch"]
         except (ValueError, KeyError, OSError):
             traffic = None
@@ -270,7 +285,7 @@ def _read_counter(folder, counter, name_filter):
 def ingest_pmc(args):
     """Scale the GEMM's FETCH_SIZE / WRITE_SIZE (KiB per dispatch) by what the
     same counters read for a plain copy of known size, and store the per-launch
-    HBM-side traffic of the dominant kernel with the kernel source hash."""
+    HBM-side traffic of the dominant kernel with the hash of its sources."""
     import paper_2608_10103_amd as mp
     gf, gw, cf, cw = args.ingest_pmc
     is_gemm = lambda n: "mpg::" in n
@@ -288,9 +303,9 @@ def ingest_pmc(args):
     v = mp.select_variant(dt, n, n, n)
     key = f"{dt}:{n}:{mp.variant_name(dt, v)}"
     hbm = (f_kib / rf + w_kib / wf) * 1024.0
-    out = {"kernel_source_hash": kernel_source_hash(),
-           "copy_calibration": {"mib": args.copy_mib_ref, "fetch_scale": rf, "write_scale": wf},
-           "points": {key: {"kernel_name": kname, "fetch_kib_per_launch": f_kib,
+    out = {"copy_calibration": {"mib": args.copy_mib_ref, "fetch_scale": rf, "write_scale": wf},
+           "points": {key: {"kernel_source_hash": kernel_source_hash(mp.variant_name(dt, v)),
+                            "kernel_name": kname, "fetch_kib_per_launch": f_kib,
                             "write_kib_per_launch": w_kib,
                             "hbm_bytes_per_launch": int(hbm)}}}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)

@@ -170,8 +170,12 @@ struct Pref { int variant; long min_tiles; };
 // INT4: the FP6 kernel once the grid has at least two 256x256 tiles per CU
 // (below that its operand conversion does not pay off), then the INT8-MFMA
 // kernels.
-const Pref kPrefF16[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+// FP16, INT8: below 256 tiles of 256 x 256 the 128-byte-slice 128 x 128
+// kernel (as fast or faster than the 64-byte one at every measured size:
+// square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
+// K does not fill 128-byte slices.
+const Pref kPrefF16[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 

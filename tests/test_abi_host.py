@@ -123,8 +123,8 @@ def test_selection_at_sweep_sizes():
         8192: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "fp6pipe256x256_w2x4_k128_s2"),
         4096: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
         2048: ("spread128x128_w2x2_k128_s4",) * 3,
-        1024: ("spread128x128_w2x2_k64_s4",) * 3,
-        512: ("spread128x128_w2x2_k64_s4",) * 3,
+        1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
+        512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
     }
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
@@ -226,3 +226,11 @@ def test_split_k_selection():
     assert L.mpgemm_select_splits(1, 999, 16, 16, 16) == -1
     assert L.mpgemm_select_splits(1, 1, -1, 16, 16) == -1
     assert L.mpgemm_select_splits(2, 1, 16, 16, 15) == -1  # odd K is not INT4
+
+
+def test_every_variant_has_a_kernel_source_family():
+    # stored counters are matched to a kernel through the hash of its sources
+    import bench
+    for dt in ("f16", "s8", "s4"):
+        for v in range(mp.num_variants(dt)):
+            assert len(bench.kernel_source_hash(mp.variant_name(dt, v))) == 16
