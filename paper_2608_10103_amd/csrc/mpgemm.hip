@@ -158,6 +158,8 @@ enum : int {
     V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
     V_PIPE64 = 13,           // pipe64x64_w1x1_k128_s4
     V_SKINNY = 38,           // skinny16x16_k64; then 16x32, 32x16, 32x32
+    V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
+    V_SKINNY64 = 43,         // skinny64x32_k64
 };
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumF16 + 1;  // fp6pipe256x256_w2x4_k128_s2
@@ -180,19 +182,24 @@ const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD1
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding). Measured on
-// MI355X against the 128x128 split-K kernel at 1..32 x {4096, 8192, 14336} x
-// {4096, 8192, 14336}: 1.2-1.7x faster for FP16 up to 16 rows (with 17..32
-// rows the tiled kernel is marginally faster), 1.1-2.1x for INT8 and 2-3x for
-// INT4 up to 32 rows. 32 large-side rows per workgroup (instead of 16) pay off
-// when each wave has at most 8 K-steps of 64 bytes or the small side needs two
-// 16-row blocks. Negative: not taken.
+// MI355X against the 128x128 split-K kernel at 1..64 x {4096, 8192, 14336} x
+// {4096, 8192, 14336}: 1.2-1.65x faster for FP16 up to 16 rows (with 17..32
+// rows the tiled kernel is marginally faster), 1.1-2.2x for INT8 up to 32
+// rows and 1.5-3x for INT4 up to 64 rows. The large side is split into groups
+// of 16 rows per workgroup, or 32 when a wave has at most 8 K-steps of 64
+// bytes or the small side needs two 16-row blocks; with exactly 8 K-steps
+// per wave, one 8-step prefetch group (skinny16x32_k64_d8) is 1.3-1.4x faster
+// than two 4-step ones. Negative: not taken.
 int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const int small = M < N ? M : N, large = M < N ? N : M;
-    if (small > (dtype == F16 ? 16 : 32) || large < 1024) return -1;
-    const int mb = small <= 16 ? 1 : 2;
+    const int most = dtype == F16 ? 16 : (dtype == S8 ? 32 : 64);
+    if (small > most || large < 1024) return -1;
     const long steps_per_wave = row_bytes(dtype, K) / 64 / SKINNY_WAVES;
-    const int nb = (mb == 2 || steps_per_wave <= 8) ? 2 : 1;
-    const int v = V_SKINNY + 2 * (mb - 1) + (nb - 1);
+    int v;
+    if (small > 32) v = V_SKINNY64;
+    else if (small > 16) v = V_SKINNY + 3;                          // 32x32
+    else if (steps_per_wave == 8) v = V_SKINNY16_D8;
+    else v = V_SKINNY + (steps_per_wave < 8 ? 1 : 0);               // 16x32 or 16x16
     return supports(dtype, table(dtype)[v], M, N, K, A, B, C) ? v : -1;
 }
 

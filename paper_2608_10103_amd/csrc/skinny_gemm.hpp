@@ -50,13 +50,13 @@ __device__ __forceinline__ void skinny_mma(i32x4 x, i32x4 w, typename SkinnyAcc<
 }
 
 constexpr int SKINNY_WAVES = 8;
-constexpr int SKINNY_DEPTH = 4;  // K-steps loaded ahead of the MFMAs
+constexpr int SKINNY_DEPTH = 4;  // default K-steps loaded ahead of the MFMAs
 
 // X: R rows (R <= 16 * MB), W: Q rows, both of Kb bytes (Kb a multiple of
 // 64). Workgroup g covers W rows [16 NB g, 16 NB (g + 1)). Output element
 // (x-row r, w-row q) goes to C(r, q) if trans == 0, C(q, r) otherwise, C
 // being row-major with `ldc` columns.
-template <int DT, int MB, int NB>
+template <int DT, int MB, int NB, int D = SKINNY_DEPTH>
 __global__ __launch_bounds__(64 * SKINNY_WAVES, 1) void skinny_gemm(const uint8_t *__restrict__ X,
                                                                    const uint8_t *__restrict__ W,
                                                                    void *__restrict__ Cv, int R, int Q,
@@ -64,7 +64,6 @@ __global__ __launch_bounds__(64 * SKINNY_WAVES, 1) void skinny_gemm(const uint8_
                                                                    EpiParams epi) {
     typedef typename SkinnyAcc<DT>::type acc_t;
     typedef typename SkinnyAcc<DT>::out out_t;
-    constexpr int D = SKINNY_DEPTH;
     constexpr int NV = 4;  // accumulator values per lane of a 16x16 block
     __shared__ __attribute__((aligned(16))) out_t part[SKINNY_WAVES][MB * NB][NV * 64];
 

@@ -107,11 +107,11 @@ Variant deep(const char *name) {
                    false};
 }
 
-template <int DT, int MB, int NB>
+template <int DT, int MB, int NB, int D = SKINNY_DEPTH>
 Variant skinny(const char *name) {
     typedef void (*skinny_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int,
                               EpiParams);
-    skinny_fn f = &skinny_gemm<DT, MB, NB>;
+    skinny_fn f = &skinny_gemm<DT, MB, NB, D>;
     return Variant{name, SKINNY, 16 * MB, 16 * NB, 64, 64 * SKINNY_WAVES, reinterpret_cast<const void *>(f),
                    false};
 }
@@ -173,11 +173,13 @@ Variant generic(const char *name) {
      skinny<DT, 1, 1>("skinny16x16_k64"),                                 \
      skinny<DT, 1, 2>("skinny16x32_k64"),                                 \
      skinny<DT, 2, 1>("skinny32x16_k64"),                                 \
-     skinny<DT, 2, 2>("skinny32x32_k64")
+     skinny<DT, 2, 2>("skinny32x32_k64"),                                 \
+     skinny<DT, 1, 2, 8>("skinny16x32_k64_d8"),                           \
+     skinny<DT, 4, 2>("skinny64x32_k64")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 42;
+constexpr int kNumCommon = 44;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -180,10 +180,10 @@ def test_fp6_variants_bound_k():
 
 
 def test_skinny_selection():
-    """At most 16 rows (FP16) or 32 rows (integers) on one side and at least
-    1024 on the other: the streaming kernel, 32 large-side rows per workgroup
-    when a wave has at most 8 K-steps of 64 bytes or the small side needs two
-    16-row blocks; never split."""
+    """At most 16 rows (FP16), 32 (INT8) or 64 (INT4) on one side and at
+    least 1024 on the other: the streaming kernel; 16 large-side rows per
+    workgroup with more than 8 K-steps of 64 bytes per wave, 32 with fewer,
+    one 8-step prefetch group with exactly 8; never split."""
     name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
     for dt in ("f16", "s8", "s4"):
         for M in (1, 7, 16):
@@ -193,15 +193,21 @@ def test_skinny_selection():
             assert mp.select_splits(dt, v, M, 8192, 8192) == 1
         assert not name(dt, 16, 1000, 8192).startswith("skinny")  # large side too small
         assert not name(dt, 16, 8192, 8192, a_ptr=(1 << 20) + 4).startswith("skinny")  # unaligned A
-    assert name("f16", 16, 8192, 8192) == "skinny16x16_k64"    # 32 K-steps per wave
-    assert name("f16", 32, 8192, 8192).startswith("spread128")  # FP16 beyond 16 rows: tiled
-    assert name("s8", 16, 8192, 8192) == "skinny16x16_k64"     # 16 K-steps per wave
-    assert name("s8", 16, 14336, 4096) == "skinny16x32_k64"    # 8 K-steps per wave
+    assert name("f16", 16, 8192, 8192) == "skinny16x16_k64"      # 32 K-steps per wave
+    assert name("f16", 16, 8192, 2048) == "skinny16x32_k64_d8"   # 8 K-steps per wave
+    assert name("f16", 32, 8192, 8192).startswith("spread128")   # FP16 beyond 16 rows: tiled
+    assert name("s8", 16, 8192, 8192) == "skinny16x16_k64"       # 16 K-steps per wave
+    assert name("s8", 16, 14336, 4096) == "skinny16x32_k64_d8"   # 8 K-steps per wave
+    assert name("s8", 16, 8192, 2048) == "skinny16x32_k64"       # 4 K-steps per wave
     assert name("s8", 32, 8192, 8192) == "skinny32x32_k64"
-    assert name("s4", 16, 8192, 8192) == "skinny16x32_k64"     # 8 K-steps per wave
-    assert name("s4", 16, 4096, 14336) == "skinny16x16_k64"    # 14 K-steps per wave
+    assert name("s8", 33, 8192, 8192).startswith("spread128")    # INT8 beyond 32 rows: tiled
+    assert name("s4", 16, 8192, 8192) == "skinny16x32_k64_d8"    # 8 K-steps per wave
+    assert name("s4", 16, 4096, 14336) == "skinny16x16_k64"      # 14 K-steps per wave
+    assert name("s4", 16, 14336, 4096) == "skinny16x32_k64"      # 4 K-steps per wave
     assert name("s4", 24, 8192, 8192) == "skinny32x32_k64"
-    assert not name("s8", 33, 8192, 8192).startswith("skinny")
+    assert name("s4", 48, 8192, 8192) == "skinny64x32_k64"
+    assert name("s4", 8192, 64, 8192) == "skinny64x32_k64"
+    assert name("s4", 65, 8192, 8192).startswith("spread128")
     assert not name("s8", 16, 8192, 8160).startswith("skinny")  # K off the 64-byte step
 
 
@@ -213,7 +219,7 @@ def test_split_k_selection():
         for n in (512, 1024, 2048, 4096, 8192):
             v = mp.select_variant(dt, n, n, n)
             assert mp.select_splits(dt, v, n, n, n) == 1
-        for M in (64, 128) + ((32,) if dt == "f16" else ()):
+        for M in (128,) + ((64,) if dt != "s4" else ()) + ((32,) if dt == "f16" else ()):
             v = mp.select_variant(dt, M, 8192, 8192)
             assert mp.variant_name(dt, v).startswith("spread128")
             assert mp.select_splits(dt, v, M, 8192, 8192) == most
