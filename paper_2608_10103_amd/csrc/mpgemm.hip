@@ -129,6 +129,16 @@ bool splits_ok(int dtype, const Variant &v, int M, int N, int K, int splits) {
     return row_bytes(dtype, K) % ((long)v.bkb * splits) == 0;
 }
 
+// Narrow-tile variants (select_narrow): three tiles with the small side on
+// A's rows, then the same three mirrored.
+constexpr int V_NARROW = 44;  // spread32x64_w1x2_k128_s4_m16, 32x128, 64x128; 64x32, 128x32, 128x64
+constexpr int kNumNarrow = 6;
+
+bool is_narrow(int dtype, const Variant &v) {
+    const Variant *t = table(dtype) + V_NARROW;
+    return &v >= t && &v < t + kNumNarrow;
+}
+
 // Splits the entry points use. Only skinny problems (M or N at most 128, the
 // LLM-inference shapes) are split: they stream one large operand from HBM,
 // and splitting K lets more CUs stream it. Measured on MI355X at M = 16,
@@ -136,16 +146,20 @@ bool splits_ok(int dtype, const Variant &v, int M, int N, int K, int splits) {
 // square problems with too few tiles the fixup (partials written back to L2
 // with a device-scope release) costs more than the extra parallelism gains
 // (N = 1024: 11 -> 15 us with 2 ranges), so they are not split. Each range
-// keeps at least 8 slices.
+// keeps at least 8 slices. The narrow tiles split only while the grid stays
+// within 128 workgroups (at 32 x 8192 x 8192 FP16 with 32 x 128 tiles:
+// 27.4 us with 2 ranges, 30.5 us with 4; INT8 with 32 x 64 tiles: 17.6 us
+// unsplit, 22.1 us with 2).
 int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
     if (!v.splitk || v.kind != TILED) return 1;
-    if (M > 128 && N > 128) return 1;
-    const int most = dtype == F16 ? 4 : 2;
+    if (M > 128 && N > 128 && !is_narrow(dtype, v)) return 1;
+    const bool narrow = is_narrow(dtype, v);
+    const int most = narrow ? 4 : (dtype == F16 ? 4 : 2);
     const long tiles = tile_count(v, M, N);
     const long slices = row_bytes(dtype, K) / v.bkb;
     int s = 1;
-    while (tiles * s < 256 && 2 * s <= most && slices % (2 * s) == 0 && slices / (2 * s) >= 8 &&
-           splits_ok(dtype, v, M, N, K, 2 * s))
+    while ((narrow ? tiles * 2 * s <= 128 : tiles * s < 256) && 2 * s <= most && slices % (2 * s) == 0 &&
+           slices / (2 * s) >= 8 && splits_ok(dtype, v, M, N, K, 2 * s))
         s *= 2;
     return s;
 }
@@ -159,7 +173,6 @@ enum : int {
     V_PIPE64 = 13,           // pipe64x64_w1x1_k128_s4
     V_SKINNY = 38,           // skinny16x16_k64; then 16x32, 32x16, 32x32
     V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
-    V_SKINNY64 = 43,         // skinny64x32_k64
 };
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumF16 + 1;  // fp6pipe256x256_w2x4_k128_s2
@@ -181,32 +194,84 @@ const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD1
 const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
-// Streaming kernel for problems with a small side (LLM decoding). Measured on
-// MI355X against the 128x128 split-K kernel at 1..64 x {4096, 8192, 14336} x
-// {4096, 8192, 14336}: 1.2-1.65x faster for FP16 up to 16 rows (with 17..32
-// rows the tiled kernel is marginally faster), 1.1-2.2x for INT8 up to 32
-// rows and 1.5-3x for INT4 up to 64 rows. The large side is split into groups
-// of 16 rows per workgroup, or 32 when a wave has at most 8 K-steps of 64
-// bytes or the small side needs two 16-row blocks; with exactly 8 K-steps
-// per wave, one 8-step prefetch group (skinny16x32_k64_d8) is 1.3-1.4x faster
-// than two 4-step ones. Negative: not taken.
+// Streaming kernel for problems with a small side (LLM decoding), against the
+// narrow tiles below (measured on MI355X at 1..32 x {4096, 8192, 14336,
+// 28672} x {4096, 8192, 14336}). It is the faster one while its workgroups
+// stay few and long: up to 8 rows (FP16) or 12 (INT8) with a large side of at
+// most 8192, 16 rows with at most 4096, 32 rows for INT4; with a larger large
+// side only when the large operand is small (at most 32 MiB: INT4 at
+// 14336 x 4096) or each wave has at least 32 K-steps (FP16 at K = 16384).
+// Up to 3.7x faster than the 128x128 split-K kernel, 1.1-1.6x faster than
+// the narrow tiles where taken, at most 1.13x slower elsewhere in its range.
+// The large side is split into groups of 16 rows per workgroup, or 32 when a
+// wave has at most 8 K-steps of 64 bytes or the small side needs two 16-row
+// blocks; with exactly 8 K-steps per wave, one 8-step prefetch group
+// (skinny16x32_k64_d8) is 1.3-1.4x faster than two 4-step ones. Negative:
+// not taken.
 int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const int small = M < N ? M : N, large = M < N ? N : M;
-    const int most = dtype == F16 ? 16 : (dtype == S8 ? 32 : 64);
+    const int most = dtype == S4 ? 32 : (large <= 4096 ? 16 : (dtype == F16 ? 8 : 12));
     if (small > most || large < 1024) return -1;
     const long steps_per_wave = row_bytes(dtype, K) / 64 / SKINNY_WAVES;
+    if (large > 8192 && (long)large * row_bytes(dtype, K) > (32l << 20) && steps_per_wave < 32) return -1;
     int v;
-    if (small > 32) v = V_SKINNY64;
-    else if (small > 16) v = V_SKINNY + 3;                          // 32x32
+    if (small > 16) v = V_SKINNY + 3;                               // 32x32
     else if (steps_per_wave == 8) v = V_SKINNY16_D8;
     else v = V_SKINNY + (steps_per_wave < 8 ? 1 : 0);               // 16x32 or 16x16
     return supports(dtype, table(dtype)[v], M, N, K, A, B, C) ? v : -1;
+}
+
+// Narrow tiles for problems with up to 256 rows on one side (LLM prefill,
+// batched decoding) and at least 1024 on the other, where the streaming
+// kernel is not taken: 32 x 64, 32 x 128 or
+// 64 x 128 tiles (small side first), and above 128 rows also the 128 x 128
+// kernel. These problems stream the operands through LDS at a per-CU rate
+// that varies little between the tiles, so the choice minimises the bytes
+// one CU copies: (tile rows of both operands) x (K range of a workgroup) x
+// (rounds of 256 workgroups). Within 10% of the minimum, long rows (at least
+// 12 KiB) take the largest tile (fewer, longer workgroups amortise the
+// per-slice overhead) and short rows the most workgroups. Measured on MI355X
+// at 1..256 x {4096, 8192, 11008, 14336, 28672} x {2048 .. 14336} against the
+// 128x128 split-K kernel: FP16 1.1-1.7x, INT8 1.1-1.5x, INT4 1.1-1.5x faster.
+// With select_skinny, the pick is within 15% of the fastest kernel measured
+// at 102 of 106 shapes (at most 1.32x slower: 48 x 11008 x 4096). Negative:
+// not taken.
+int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
+    const int small = M < N ? M : N, large = M < N ? N : M;
+    if (small > 256 || large < 1024) return -1;
+    const Variant *t = table(dtype);
+    const long kb = row_bytes(dtype, K);
+    int cands[4], nc = 0;
+    for (int i = 0; i < 3; ++i) cands[nc++] = V_NARROW + i + (M <= N ? 0 : 3);
+    if (small > 128) cands[nc++] = V_SPREAD128_K128;
+    int best = -1;
+    double best_cost = 0, costs[4];
+    long wgs[4];
+    for (int i = 0; i < nc; ++i) {
+        const Variant &v = t[cands[i]];
+        costs[i] = -1;
+        if (!supports(dtype, v, M, N, K, A, B, C)) continue;
+        const int sp = choose_splits(dtype, v, M, N, K);
+        wgs[i] = tile_count(v, M, N) * sp;
+        costs[i] = (double)((wgs[i] + 255) / 256) * (v.bm + v.bn) * kb / sp;
+        if (best < 0 || costs[i] < best_cost) best = i, best_cost = costs[i];
+    }
+    if (best < 0) return -1;
+    for (int i = 0; i < nc; ++i) {
+        if (costs[i] < 0 || costs[i] > 1.1 * best_cost || i == best) continue;
+        const Variant &v = t[cands[i]], &b = t[cands[best]];
+        const bool bigger = (long)v.bm * v.bn > (long)b.bm * b.bn;
+        if (kb >= 12288 ? bigger : (wgs[i] > wgs[best] || (wgs[i] == wgs[best] && bigger))) best = i;
+    }
+    return cands[best];
 }
 
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const Variant *t = table(dtype);
     const int sk = select_skinny(dtype, M, N, K, A, B, C);
     if (sk >= 0) return sk;
+    const int nv = select_narrow(dtype, M, N, K, A, B, C);
+    if (nv >= 0) return nv;
     // Skinny problems (M or N at most 128: LLM-inference shapes) are bound by
     // streaming the large operand from HBM; the 4-wave 128x128 pipelined
     // kernel with split-K keeps every CU streaming, and the padding rows it

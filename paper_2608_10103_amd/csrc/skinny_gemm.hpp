@@ -1,12 +1,12 @@
-// skinny_gemm.hpp - GEMMs with at most 32 rows on one side (LLM decoding:
-// a few tokens times a weight matrix).
+// skinny_gemm.hpp - GEMMs with at most 16 * MB rows on one side (LLM
+// decoding: a few tokens times a weight matrix).
 //
 // Such a product is bound by streaming the large operand once from HBM; the
 // tiled kernels pad the small side to a 128-row tile and finish each tile's
 // K range too quickly for their pipeline to reach full bandwidth. This kernel
 // streams instead:
 //
-//  * The small operand ("X": R <= 32 rows of K, K-contiguous) is padded to
+//  * The small operand ("X": R <= 16 MB rows of K, K-contiguous) is padded to
 //    16-row blocks, read from L2 straight into registers.
 //  * The large operand ("W": Q rows of K, K-contiguous) is split into groups
 //    of 16 * NB rows, one workgroup per group; the 8 waves of a workgroup split

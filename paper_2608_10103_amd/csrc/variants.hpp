@@ -37,6 +37,13 @@ typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 4, 4> T256x256_w8_k64_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 3, 4> T256x256_w8_k64_s3;
 typedef TileCfg<256, 256, 2, 2, 64, 5, 4> T256x256_w4_k64_s5;
+// narrow tiles for 17..256 rows on one side (A side first, then mirrored)
+typedef TileCfg<32, 64, 1, 2, 128, 4, 4, 16> T32x64_w2_m16;
+typedef TileCfg<32, 128, 1, 4, 128, 4, 4, 16> T32x128_w4_m16;
+typedef TileCfg<64, 128, 2, 2, 128, 4, 4> T64x128_w4;
+typedef TileCfg<64, 32, 2, 1, 128, 4, 4, 16> T64x32_w2_m16;
+typedef TileCfg<128, 32, 4, 1, 128, 4, 4, 16> T128x32_w4_m16;
+typedef TileCfg<128, 64, 2, 2, 128, 4, 4> T128x64_w4;
 
 //             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
 typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
@@ -175,11 +182,17 @@ Variant generic(const char *name) {
      skinny<DT, 2, 1>("skinny32x16_k64"),                                 \
      skinny<DT, 2, 2>("skinny32x32_k64"),                                 \
      skinny<DT, 1, 2, 8>("skinny16x32_k64_d8"),                           \
-     skinny<DT, 4, 2>("skinny64x32_k64")
+     skinny<DT, 4, 2>("skinny64x32_k64"),                                 \
+     pipelined<DT, T32x64_w2_m16, true>("spread32x64_w1x2_k128_s4_m16"),  \
+     pipelined<DT, T32x128_w4_m16, true>("spread32x128_w1x4_k128_s4_m16"), \
+     pipelined<DT, T64x128_w4, true>("spread64x128_w2x2_k128_s4"),        \
+     pipelined<DT, T64x32_w2_m16, true>("spread64x32_w2x1_k128_s4_m16"),  \
+     pipelined<DT, T128x32_w4_m16, true>("spread128x32_w4x1_k128_s4_m16"), \
+     pipelined<DT, T128x64_w4, true>("spread128x64_w2x2_k128_s4")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 44;
+constexpr int kNumCommon = 50;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

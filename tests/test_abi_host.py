@@ -180,52 +180,94 @@ def test_fp6_variants_bound_k():
 
 
 def test_skinny_selection():
-    """At most 16 rows (FP16), 32 (INT8) or 64 (INT4) on one side and at
-    least 1024 on the other: the streaming kernel; 16 large-side rows per
-    workgroup with more than 8 K-steps of 64 bytes per wave, 32 with fewer,
-    one 8-step prefetch group with exactly 8; never split."""
+    """The streaming kernel while its workgroups stay few and long: up to 8
+    rows (FP16) or 12 (INT8) on the small side with 1024..8192 on the large
+    one, 16 rows with at most 4096, 32 rows for INT4; with a larger large side
+    only for a large operand of at most 32 MiB or at least 32 K-steps per wave.
+    16 large-side rows per workgroup with more than 8 K-steps of 64 bytes per
+    wave, 32 with fewer, one 8-step prefetch group with exactly 8; never
+    split."""
     name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
     for dt in ("f16", "s8", "s4"):
-        for M in (1, 7, 16):
+        for M in (1, 7, 8):
             assert name(dt, M, 8192, 8192).startswith("skinny16x"), (dt, M)
             assert name(dt, 8192, M, 8192).startswith("skinny16x"), (dt, M)  # small N: operands swapped
             v = mp.select_variant(dt, M, 8192, 8192)
             assert mp.select_splits(dt, v, M, 8192, 8192) == 1
+        assert name(dt, 16, 4096, 4096).startswith("skinny16x")
         assert not name(dt, 16, 1000, 8192).startswith("skinny")  # large side too small
-        assert not name(dt, 16, 8192, 8192, a_ptr=(1 << 20) + 4).startswith("skinny")  # unaligned A
-    assert name("f16", 16, 8192, 8192) == "skinny16x16_k64"      # 32 K-steps per wave
-    assert name("f16", 16, 8192, 2048) == "skinny16x32_k64_d8"   # 8 K-steps per wave
-    assert name("f16", 32, 8192, 8192).startswith("spread128")   # FP16 beyond 16 rows: tiled
-    assert name("s8", 16, 8192, 8192) == "skinny16x16_k64"       # 16 K-steps per wave
-    assert name("s8", 16, 14336, 4096) == "skinny16x32_k64_d8"   # 8 K-steps per wave
-    assert name("s8", 16, 8192, 2048) == "skinny16x32_k64"       # 4 K-steps per wave
-    assert name("s8", 32, 8192, 8192) == "skinny32x32_k64"
-    assert name("s8", 33, 8192, 8192).startswith("spread128")    # INT8 beyond 32 rows: tiled
+        assert not name(dt, 8, 8192, 8192, a_ptr=(1 << 20) + 4).startswith("skinny")  # unaligned A
+    assert name("f16", 8, 8192, 8192) == "skinny16x16_k64"       # 32 K-steps per wave
+    assert name("f16", 8, 8192, 2048) == "skinny16x32_k64_d8"    # 8 K-steps per wave
+    assert not name("f16", 9, 8192, 8192).startswith("skinny")
+    assert name("s8", 12, 8192, 8192) == "skinny16x16_k64"       # 16 K-steps per wave
+    assert not name("s8", 13, 8192, 8192).startswith("skinny")
+    assert name("s8", 16, 4096, 4096) == "skinny16x32_k64_d8"    # 8 K-steps per wave
+    assert name("s8", 16, 4096, 2048) == "skinny16x32_k64"       # 4 K-steps per wave
     assert name("s4", 16, 8192, 8192) == "skinny16x32_k64_d8"    # 8 K-steps per wave
     assert name("s4", 16, 4096, 14336) == "skinny16x16_k64"      # 14 K-steps per wave
-    assert name("s4", 16, 14336, 4096) == "skinny16x32_k64"      # 4 K-steps per wave
+    assert name("s4", 16, 14336, 4096) == "skinny16x32_k64"      # 4 K-steps; 28 MiB large operand
     assert name("s4", 24, 8192, 8192) == "skinny32x32_k64"
-    assert name("s4", 48, 8192, 8192) == "skinny64x32_k64"
-    assert name("s4", 8192, 64, 8192) == "skinny64x32_k64"
-    assert name("s4", 65, 8192, 8192).startswith("spread128")
+    assert name("s4", 8192, 32, 8192) == "skinny32x32_k64"
+    # a large side beyond 8192: only a small large operand or long waves
+    assert not name("f16", 1, 14336, 4096).startswith("skinny")  # 112 MiB, 16 K-steps per wave
+    assert not name("s8", 1, 14336, 4096).startswith("skinny")   # 56 MiB, 8 K-steps per wave
+    assert not name("s4", 1, 28672, 8192).startswith("skinny")   # 112 MiB, 8 K-steps per wave
+    assert name("f16", 4, 28672, 8192) == "skinny16x16_k64"      # 32 K-steps per wave
     assert not name("s8", 16, 8192, 8160).startswith("skinny")  # K off the 64-byte step
 
 
+def test_narrow_selection():
+    """17..256 rows on one side (past the streaming kernel) and at least 1024
+    on the other: the narrow tiles, small side first; mirrored when N is the
+    small side."""
+    name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
+    # the tile that copies the fewest bytes per CU (32 x 128: 64 tiles, 2
+    # K-ranges; 32 x 64: 128 tiles; 64 x 128: 64 tiles, 2 K-ranges)
+    assert name("f16", 16, 8192, 8192) == "spread32x128_w1x4_k128_s4_m16"
+    assert name("f16", 32, 8192, 8192) == "spread32x128_w1x4_k128_s4_m16"
+    assert name("f16", 1, 14336, 4096) == "spread32x64_w1x2_k128_s4_m16"   # 224 tiles
+    assert name("s8", 32, 14336, 4096) == "spread32x64_w1x2_k128_s4_m16"
+    assert name("s4", 64, 8192, 8192) == "spread32x64_w1x2_k128_s4_m16"    # 256 tiles
+    assert name("f16", 64, 4096, 14336) == "spread64x128_w2x2_k128_s4"     # 32 tiles, 4 K-ranges
+    for dt in ("f16", "s8", "s4"):
+        assert name(dt, 128, 8192, 8192) == "spread32x128_w1x4_k128_s4_m16"
+        assert name(dt, 8192, 128, 8192) == "spread128x32_w4x1_k128_s4_m16"  # small N: mirrored
+        assert name(dt, 256, 8192, 8192) == "spread64x128_w2x2_k128_s4"
+        assert name(dt, 8192, 256, 8192) == "spread128x64_w2x2_k128_s4"
+        assert name(dt, 256, 14336, 4096) == "spread128x128_w2x2_k128_s4"   # 224 tiles beat 448
+        assert not name(dt, 257, 8192, 8192).startswith(("spread32", "spread64"))
+        assert name(dt, 64, 1000, 8192).startswith("spread128")  # large side too small
+        assert name(dt, 64, 8192, 8192 - 8).startswith("generic") or \
+            name(dt, 64, 8192, 8192 - 8).startswith("spread128")  # K off the 128-byte slice
+    assert name("s8", 8192, 64, 8192) == "spread64x32_w2x1_k128_s4_m16"
+
+
 def test_split_k_selection():
-    """Only problems with M or N <= 128 that the streaming kernel does not
-    take are split; FP16 up to 4 K-ranges, integers up to 2; square sweep
+    """Only problems with M or N <= 128 that neither the streaming kernel nor
+    the narrow tiles take, and the narrow tiles themselves, are split: the
+    128x128 tiles up to 256 workgroups (FP16 up to 4 K-ranges, integers up to
+    2), the narrow tiles up to 128 workgroups and 4 K-ranges; square sweep
     sizes never."""
     for dt, most in (("f16", 4), ("s8", 2), ("s4", 2)):
         for n in (512, 1024, 2048, 4096, 8192):
             v = mp.select_variant(dt, n, n, n)
             assert mp.select_splits(dt, v, n, n, n) == 1
-        for M in (128,) + ((64,) if dt != "s4" else ()) + ((32,) if dt == "f16" else ()):
-            v = mp.select_variant(dt, M, 8192, 8192)
+        for M in (64, 128):
+            v = mp.select_variant(dt, M, 1000, 8192)  # large side too small for the narrow tiles
             assert mp.variant_name(dt, v).startswith("spread128")
-            assert mp.select_splits(dt, v, M, 8192, 8192) == most
-            assert mp.select_splits(dt, v, 8192, M, 8192) == most
+            assert mp.select_splits(dt, v, M, 1000, 8192) == most
         v = mp.select_variant(dt, 64, 8192, 1024)
         assert mp.select_splits(dt, v, 64, 8192, 1024) <= most  # every range keeps >= 8 slices
+    sel = lambda dt, M, N, K: mp.select_splits(dt, mp.select_variant(dt, M, N, K), M, N, K)
+    assert sel("f16", 32, 8192, 8192) == 2     # 64 tiles of 32 x 128
+    assert sel("f16", 8192, 32, 8192) == 2
+    assert sel("f16", 64, 8192, 8192) == 2     # 64 tiles of 64 x 128
+    assert sel("f16", 64, 4096, 8192) == 4     # 32 tiles
+    assert sel("s8", 32, 8192, 8192) == 2      # 64 tiles of 32 x 128
+    assert sel("s8", 32, 14336, 4096) == 1     # 224 tiles of 32 x 64
+    assert sel("s8", 128, 8192, 8192) == 1
+    assert sel("f16", 256, 8192, 8192) == 1
     assert mp.select_splits("s8", 0, 16, 8192, 8192) == 1  # the bounds-checked kernel never splits
     L = mp.lib()
     assert L.mpgemm_select_splits(7, 1, 16, 16, 16) == -1

@@ -432,7 +432,9 @@ def test_llm_inference_shapes(dtype):
     """Skinny GEMMs of LLM inference (M tokens x N outputs x K inputs) through
     the entry point, whatever kernel and split it picks."""
     for (M, N, K) in [(1, 4096, 4096), (16, 4096, 4096), (64, 8192, 4096), (128, 4096, 8192),
-                      (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048)]:
+                      (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048),
+                      # the narrow tiles, mirrored when N is the small side
+                      (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
         C = gpu_gemm(dtype, A, B)
         v = mp.select_variant(dtype, M, N, K)
