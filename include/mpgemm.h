@@ -46,7 +46,8 @@
  *                         pointer NULL (A and B when M, N, K > 0; C when
  *                         M, N > 0); C overlapping A or B; a problem whose
  *                         element counts overflow 64-bit byte offsets;
- *   hipErrorOutOfMemory   (INT4) the workspace could not be allocated, or
+ *   hipErrorOutOfMemory   a workspace (INT4 on the FP6 cores; split K, see
+ *                         mpgemm_select_splits) could not be allocated, or
  *                         the error of synchronising the stream to grow it;
  *   the launch error      if a kernel launch itself fails.
  * Nothing is enqueued when an argument error is returned.
@@ -179,9 +180,11 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
  * Partials and per-tile counters live in a per-(device, stream) workspace
  * like the FP6 one (allocated on first use, grown after synchronising the
  * stream, counters zeroed on the stream when allocated, kept until the
- * process ends). The entry points split only skinny problems (M or N at
- * most 128) whose tile grid has fewer than 256 tiles: up to 4 ranges for
- * FP16, 2 for the integer types. */
+ * process ends). The entry points split only problems with a small side:
+ * the narrow tiles (at most 256 rows on one side, at least 1024 on the other)
+ * while the grid stays within 128 workgroups, up to 4 ranges; where those do
+ * not apply, the 128x128 tiles of problems with M or N at most 128 up to 256
+ * workgroups, 4 ranges for FP16, 2 for the integer types. */
 
 /* Splits the entry points use for this variant and problem (1 = none), or -1
  * for an invalid dtype, variant or size. */
