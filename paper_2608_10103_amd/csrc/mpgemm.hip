@@ -99,6 +99,14 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
         if (dtype == S4 && K >= 131072) return false;  // INT4 sums carried times 256
         return true;
     }
+    if (v.kind == WIDE) {
+        // whole 256 x 256 tiles and 128-byte K-slices, 16-byte aligned rows;
+        // the copy buffers span 128 rows of K bytes (32-bit range)
+        if (!v.fn || M % v.bm || N % v.bn) return false;
+        const long kb = row_bytes(dtype, K);
+        if (kb % v.bkb || 128 * kb > INT_MAX) return false;
+        return aligned(A, 16) && aligned(B, 16);
+    }
     if (v.kind == FP6) {
         if (dtype != S4) return false;
         if (F6Geom::runs_pad(K) * 32 > kF6MaxK) return false;
@@ -167,6 +175,7 @@ int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
 // Variant indices in the tables above that the selection uses.
 enum : int {
     V_PIPE256_W2X4 = 9,      // pipe256x256_w2x4_k128_s2
+    V_WIDE = 50,             // wide256x256_w2x2_k128_m16
     V_SPREAD128_K128 = 20,   // spread128x128_w2x2_k128_s4
     V_SPREAD128_K64 = 21,    // spread128x128_w2x2_k64_s4
     V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
@@ -189,7 +198,10 @@ struct Pref { int variant; long min_tiles; };
 // kernel (as fast or faster than the 64-byte one at every measured size:
 // square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
 // K does not fill 128-byte slices.
-const Pref kPrefF16[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+// FP16: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles fill
+// the CUs (1.03-1.14x the 8-wave kernel at 4096..8192 x 4096..16384 x
+// 2048..8192; for INT8 it wins only at 8192^3, by 4%, and is not selected).
+const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};

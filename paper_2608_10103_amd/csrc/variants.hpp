@@ -12,6 +12,7 @@
 #include "f6_gemm.hpp"
 #include "deep_gemm.hpp"
 #include "skinny_gemm.hpp"
+#include "wide_gemm.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -59,7 +60,7 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4 };
 
 struct Variant {
     const char *name;
@@ -121,6 +122,18 @@ Variant skinny(const char *name) {
     skinny_fn f = &skinny_gemm<DT, MB, NB, D>;
     return Variant{name, SKINNY, 16 * MB, 16 * NB, 64, 64 * SKINNY_WAVES, reinterpret_cast<const void *>(f),
                    false};
+}
+
+// One wave per SIMD, 256 x 256 tiles only (wide_gemm.hpp); FP16 and INT8 (no
+// kernel for INT4: fn is null and the variant supports nothing).
+template <int DT>
+Variant wide(const char *name) {
+    const void *f = nullptr;
+    if constexpr (DT == F16 || DT == S8) {
+        kernel_fn k = &wide_gemm<DT>;
+        f = reinterpret_cast<const void *>(k);
+    }
+    return Variant{name, WIDE, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false};
 }
 
 template <class T>
@@ -188,11 +201,12 @@ Variant generic(const char *name) {
      pipelined<DT, T64x128_w4, true>("spread64x128_w2x2_k128_s4"),        \
      pipelined<DT, T64x32_w2_m16, true>("spread64x32_w2x1_k128_s4_m16"),  \
      pipelined<DT, T128x32_w4_m16, true>("spread128x32_w4x1_k128_s4_m16"), \
-     pipelined<DT, T128x64_w4, true>("spread128x64_w2x2_k128_s4")
+     pipelined<DT, T128x64_w4, true>("spread128x64_w2x2_k128_s4"),        \
+     wide<DT>("wide256x256_w2x2_k128_m16")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 50;
+constexpr int kNumCommon = 51;
 constexpr int kNumFp6 = 8;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -34,7 +34,7 @@ def test_variant_table():
         n = mp.num_variants(dt)
         assert n >= 2
         assert mp.variant_name(dt, 0).startswith("generic")
-        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny") + (("fp6pipe",) if dt == "s4" else ())
+        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny", "wide") + (("fp6pipe",) if dt == "s4" else ())
         assert all(mp.variant_name(dt, v).startswith(prefixes) for v in range(1, n))
         assert mp.variant_name(dt, n) == ""
     assert mp.lib().mpgemm_num_variants(7) == -1
@@ -120,8 +120,8 @@ def test_lds_swizzle_is_a_permutation(ch):
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
-        8192: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "fp6pipe256x256_w2x4_k128_s2"),
-        4096: ("pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
+        8192: ("wide256x256_w2x2_k128_m16", "pipe256x256_w2x4_k128_s2", "fp6pipe256x256_w2x4_k128_s2"),
+        4096: ("wide256x256_w2x2_k128_m16", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
         2048: ("spread128x128_w2x2_k128_s4",) * 3,
         1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
         512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
@@ -129,6 +129,8 @@ def test_selection_at_sweep_sizes():
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
         assert got == names, (n, got)
+    # FP16 off whole 256 x 256 tiles: the 8-wave kernel with predicated edges
+    assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "pipe256x256_w2x4_k128_s2"
 
 
 def _e3m2_value(c):
@@ -282,3 +284,19 @@ def test_every_variant_has_a_kernel_source_family():
     for dt in ("f16", "s8", "s4"):
         for v in range(mp.num_variants(dt)):
             assert len(bench.kernel_source_hash(mp.variant_name(dt, v))) == 16
+
+
+def test_wide_variant_support():
+    """The one-wave-per-SIMD kernel takes whole 256 x 256 tiles and 128-byte
+    K-slices of 16-byte aligned FP16 or INT8 operands, nothing else."""
+    for dt, e in (("f16", 64), ("s8", 128), ("s4", 256)):
+        v = [i for i in range(mp.num_variants(dt)) if mp.variant_name(dt, i) == "wide256x256_w2x2_k128_m16"]
+        assert len(v) == 1
+        v = v[0]
+        ok = dt != "s4"
+        assert mp.variant_supports(dt, v, 256, 256, e) == ok
+        assert mp.variant_supports(dt, v, 8192, 4096, 64 * e) == ok
+        assert not mp.variant_supports(dt, v, 257, 256, e)       # ragged M
+        assert not mp.variant_supports(dt, v, 256, 200, e)       # ragged N
+        assert not mp.variant_supports(dt, v, 256, 256, e + 2)   # K off the slice
+        assert not mp.variant_supports(dt, v, 256, 256, e, a_ptr=(1 << 20) + 4)  # unaligned A
