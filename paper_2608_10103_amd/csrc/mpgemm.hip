@@ -433,8 +433,14 @@ hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, 
     int kb = (int)row_bytes(dtype, K);
     int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
     if (!v.splitk) {
+        const void *fn = v.fn;
+        // the one-wave-per-SIMD kernel's table entry stores raw sums; scaled
+        // outputs take its instantiation with the shared epilogue
+        if (v.kind == WIDE && epi.out != OUT_PLAIN)
+            fn = dtype == F16 ? reinterpret_cast<const void *>(&wide_gemm<F16, false>)
+                              : reinterpret_cast<const void *>(&wide_gemm<S8, false>);
         void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &epi};
-        return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+        return hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
     int *counters = nullptr;
     uint32_t *partials = nullptr;

@@ -118,7 +118,10 @@ __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b
     });
 }
 
-template <int DT>
+// PLAIN: raw sums to the row-major output (the entry points' common case),
+// stored straight from the accumulators; otherwise the shared epilogue with
+// scales, zero points and output types (see EpiParams).
+template <int DT, bool PLAIN = true>
 __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t *__restrict__ A,
                                                                  const uint8_t *__restrict__ B,
                                                                  void *__restrict__ Cv, int M, int N, int Kb,
@@ -153,6 +156,15 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[i][j] = acc_t{};
+    // The zeroed accumulators are written to the AGPRs here (each empty asm
+    // takes its block in AGPRs, in order), then wait states before the first
+    // assembly MFMA reads them: the compiler does not insert them for
+    // assembly it does not know is an MFMA.
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
+    asm volatile("s_nop 4" ::: "memory");
 
     const int KT = Kb / T::BKB;
     // prologue: slice 0 whole, loads 0-11 of slice 1; wait for slice 0
@@ -185,7 +197,22 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
 
     const long row0 = (long)tm * T::BM + wm * 128;
     const long col0 = (long)tn * T::BN + wn * 128 + r;
-    epi_store_tile<DT, 16, 8, 8, 4>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
+    if constexpr (PLAIN) {
+        // whole tiles: element (i, j, v) of this lane is row row0 + 16 i +
+        // 4 h + v, column col0 + 16 j
+        typedef typename Acc<DT, 16>::out out_t;
+        out_t *base = reinterpret_cast<out_t *>(Cv) + (row0 + 4 * h) * (long)N + col0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                out_t *rowp = base + (long)(16 * i + v) * N;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) rowp[16 * j] = acc[i][j][v];
+            }
+    } else {
+        epi_store_tile<DT, 16, 8, 8, 4>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
+    }
 }
 
 }  // namespace mpg
