@@ -202,7 +202,7 @@ struct Pref { int variant; long min_tiles; };
 // the CUs (1.03-1.14x the 8-wave kernel at 4096..8192 x 4096..16384 x
 // 2048..8192; for INT8 it wins only at 8192^3, by 4%, and is not selected).
 const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS8[] = {{V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 

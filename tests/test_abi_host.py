@@ -120,8 +120,8 @@ def test_lds_swizzle_is_a_permutation(ch):
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
-        8192: ("wide256x256_w2x2_k128_m16", "pipe256x256_w2x4_k128_s2", "fp6pipe256x256_w2x4_k128_s2"),
-        4096: ("wide256x256_w2x2_k128_m16", "pipe256x256_w2x4_k128_s2", "staged256x256_w2x4_k128_n1"),
+        8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6pipe256x256_w2x4_k128_s2",),
+        4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("staged256x256_w2x4_k128_n1",),
         2048: ("spread128x128_w2x2_k128_s4",) * 3,
         1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
         512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
