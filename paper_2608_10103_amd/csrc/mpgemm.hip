@@ -198,9 +198,10 @@ struct Pref { int variant; long min_tiles; };
 // kernel (as fast or faster than the 64-byte one at every measured size:
 // square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
 // K does not fill 128-byte slices.
-// FP16: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles fill
-// the CUs (1.03-1.14x the 8-wave kernel at 4096..8192 x 4096..16384 x
-// 2048..8192; for INT8 it wins only at 8192^3, by 4%, and is not selected).
+// FP16, INT8: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles
+// fill the CUs (1.09-1.21x the 8-wave kernel for FP16, 1.12-1.23x for INT8,
+// at 2048..16384 x 4096..16384 x 2048..16384); the 8-wave kernel, with
+// predicated edges, where M or N is not a multiple of 256.
 const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
