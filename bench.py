@@ -70,7 +70,8 @@ KERNEL_SOURCES = {"generic": ["generic_gemm.hpp"], "tile": ["tiled_gemm.hpp"], "
                   "spread": ["tiled_gemm.hpp"], "staged": ["tiled_gemm.hpp"],
                   "pingpong": ["tiled_gemm.hpp"], "fp6pipe": ["tiled_gemm.hpp", "f6_gemm.hpp"],
                   "deep": ["tiled_gemm.hpp", "deep_gemm.hpp"], "skinny": ["skinny_gemm.hpp"],
-                  "wide": ["tiled_gemm.hpp", "wide_gemm.hpp"]}
+                  "wide": ["tiled_gemm.hpp", "wide_gemm.hpp"],
+                  "fp6wide": ["tiled_gemm.hpp", "f6_gemm.hpp", "wide_gemm.hpp", "wide_f6.hpp"]}
 
 
 def kernel_source_hash(variant_name: str) -> str:

@@ -107,10 +107,16 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
         if (kb % v.bkb || 128 * kb > INT_MAX) return false;
         return aligned(A, 16) && aligned(B, 16);
     }
-    if (v.kind == FP6) {
+    if (v.kind == FP6 || v.kind == FP6WIDE) {
         if (dtype != S4) return false;
         if (F6Geom::runs_pad(K) * 32 > kF6MaxK) return false;
-        return F6Geom::rows_pad(M) <= kF6MaxRows && F6Geom::rows_pad(N) <= kF6MaxRows;
+        if (F6Geom::rows_pad(M) > kF6MaxRows || F6Geom::rows_pad(N) > kF6MaxRows) return false;
+        // the one-wave-per-SIMD kernel addresses each workspace part (P: 16
+        // bytes per row and run) with 32-bit byte offsets
+        if (v.kind == FP6WIDE)
+            return F6Geom::runs_pad(K) * 16 * (F6Geom::rows_pad(M) > F6Geom::rows_pad(N) ? F6Geom::rows_pad(M)
+                                                                                          : F6Geom::rows_pad(N)) <= INT_MAX;
+        return true;
     }
     const long kb = row_bytes(dtype, K);
     // edge tiles are predicated in M and N; K must fill whole slices
@@ -185,14 +191,18 @@ enum : int {
 };
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumF16 + 1;  // fp6pipe256x256_w2x4_k128_s2
+constexpr int V_FP6_WIDE = kNumF16 + 8;    // fp6wide256x256_w2x2_k128_s3
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
 // taken when it supports the problem and yields at least `min_tiles`
 // workgroups (256 = one per CU). Chosen from interleaved timings of every
 // variant at N = 512 ... 8192 on MI355X.
 struct Pref { int variant; long min_tiles; };
-// INT4: the FP6 kernel once the grid has at least two 256x256 tiles per CU
-// (below that its operand conversion does not pay off), then the INT8-MFMA
+// INT4: the one-wave-per-SIMD FP6 kernel once 256 x 256 tiles fill the CUs
+// (1.10x the INT8-MFMA kernel at 4096^3 with the conversion counted, 1.14-
+// 1.19x the 8-wave FP6 kernel at 4096..16384 x 8192 x 2048..16384; below
+// 256 tiles the conversion does not pay off), the 8-wave FP6 kernel where
+// the first's 32-bit workspace offsets do not reach, then the INT8-MFMA
 // kernels.
 // FP16, INT8: below 256 tiles of 256 x 256 the 128-byte-slice 128 x 128
 // kernel (as fast or faster than the 64-byte one at every measured size:
@@ -204,7 +214,7 @@ struct Pref { int variant; long min_tiles; };
 // predicated edges, where M or N is not a multiple of 256.
 const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
+const Pref kPrefS4[] = {{V_FP6_WIDE, 256}, {V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
                         {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the
@@ -406,8 +416,13 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
         int32_t *c = static_cast<int32_t *>(C);
         int ma = (int)Ma, nb = (int)Nb, kt = (int)(runs / v.bkb);
         int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
+        // the one-wave-per-SIMD kernel's table entry stores raw sums of whole
+        // tiles; ragged or scaled outputs take its shared-epilogue instantiation
+        const void *fn = v.fn;
+        if (v.kind == FP6WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn))
+            fn = reinterpret_cast<const void *>(&wide_f6_gemm<false>);
         void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &epi};
-        e = hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+        e = hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
     return e;
 }
@@ -416,7 +431,7 @@ hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, 
                   const void *B, void *C, EpiParams epi, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
-    if (v.kind == FP6) return launch_fp6(v, M, N, K, a, b, C, epi, stream);
+    if (v.kind == FP6 || v.kind == FP6WIDE) return launch_fp6(v, M, N, K, a, b, C, epi, stream);
     if (v.kind == SKINNY) {
         // X = the operand with at most bm rows (A when M is small), W = the other
         int trans = M <= v.bm ? 0 : 1;

@@ -13,6 +13,7 @@
 #include "deep_gemm.hpp"
 #include "skinny_gemm.hpp"
 #include "wide_gemm.hpp"
+#include "wide_f6.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -60,7 +61,7 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5 };
 
 struct Variant {
     const char *name;
@@ -145,6 +146,16 @@ Variant fp6(const char *name) {
                    false};
 }
 
+// The one-wave-per-SIMD FP6 kernel (wide_f6.hpp); the table holds its
+// raw-sum instantiation, the launcher swaps in the other where needed.
+inline Variant fp6wide(const char *name) {
+    typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
+                          int32_t *, int, int, int, int, int, int, int, EpiParams);
+    f6_fn f = &wide_f6_gemm<true>;
+    return Variant{name, FP6WIDE, WideF6Cfg::BM, WideF6Cfg::BN, WideF6Cfg::J, WideF6Cfg::NTHREADS,
+                   reinterpret_cast<const void *>(f), false};
+}
+
 template <int DT>
 Variant generic(const char *name) {
     generic_fn f = &generic_gemm<DT>;
@@ -207,7 +218,7 @@ Variant generic(const char *name) {
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
 constexpr int kNumCommon = 51;
-constexpr int kNumFp6 = 8;
+constexpr int kNumFp6 = 9;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 
 // Kernel of the transposed-B entry point (tposeb.hip): F16 or S8, else null.

@@ -12,7 +12,8 @@ const Variant kS4[] = {VARIANT_LIST(S4),
                              fp6<F6_256x128_w4_s4>("fp6pipe256x128_w2x2_k128_s4"),
                              fp6<F6_128x128_w4_s4>("fp6pipe128x128_w2x2_k128_s4"),
                              fp6<F6_128x128_w4_s6>("fp6pipe128x128_w2x2_k128_s6"),
-                             fp6<F6_128x128_w4_k256_s3>("fp6pipe128x128_w2x2_k256_s3")};
+                             fp6<F6_128x128_w4_k256_s3>("fp6pipe128x128_w2x2_k256_s3"),
+                             fp6wide("fp6wide256x256_w2x2_k128_s3")};
 static_assert(sizeof(kS4) / sizeof(kS4[0]) == kNumS4, "variant count out of date in variants.hpp");
 
 }  // namespace mpg

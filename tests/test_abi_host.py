@@ -34,7 +34,7 @@ def test_variant_table():
         n = mp.num_variants(dt)
         assert n >= 2
         assert mp.variant_name(dt, 0).startswith("generic")
-        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny", "wide") + (("fp6pipe",) if dt == "s4" else ())
+        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny", "wide") + (("fp6pipe", "fp6wide") if dt == "s4" else ())
         assert all(mp.variant_name(dt, v).startswith(prefixes) for v in range(1, n))
         assert mp.variant_name(dt, n) == ""
     assert mp.lib().mpgemm_num_variants(7) == -1
@@ -120,8 +120,8 @@ def test_lds_swizzle_is_a_permutation(ch):
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
-        8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6pipe256x256_w2x4_k128_s2",),
-        4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("staged256x256_w2x4_k128_n1",),
+        8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6wide256x256_w2x2_k128_s3",),
+        4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6wide256x256_w2x2_k128_s3",),
         2048: ("spread128x128_w2x2_k128_s4",) * 3,
         1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
         512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
@@ -179,6 +179,22 @@ def test_fp6_variants_bound_k():
         assert not mp.variant_supports("s4", v, 64, 64, 3)  # odd K is not INT4
     for dt in ("f16", "s8"):
         assert not any(mp.variant_name(dt, v).startswith("fp6") for v in range(mp.num_variants(dt)))
+
+
+def test_fp6_wide_workspace_offset_bound():
+    """The one-wave-per-SIMD FP6 kernel addresses each workspace part with
+    32-bit byte offsets: 16 bytes per padded row and 32-k run of the larger
+    operand must stay within 2^31 - 1; beyond that the 8-wave FP6 kernel
+    takes the problem."""
+    names = [mp.variant_name("s4", v) for v in range(mp.num_variants("s4"))]
+    wide, pipe = names.index("fp6wide256x256_w2x2_k128_s3"), names.index("fp6pipe256x256_w2x4_k128_s2")
+    # 65536 rows x 4096 runs x 16 bytes = 2^32: too far; 2^30 fits
+    assert not mp.variant_supports("s4", wide, 65536, 256, 1 << 17)
+    assert not mp.variant_supports("s4", wide, 256, 65536, 1 << 17)
+    assert mp.variant_supports("s4", pipe, 65536, 256, 1 << 17)
+    assert mp.variant_supports("s4", wide, 16384, 256, 1 << 17)
+    assert mp.select_variant("s4", 65536, 4096, 1 << 17) == pipe
+    assert mp.select_variant("s4", 16384, 4096, 1 << 17) == wide
 
 
 def test_skinny_selection():
