@@ -12,7 +12,10 @@ the fraction of the variant's MFMA peak and whether its output equals the
 first variant's (integers) or is within 1e-3 relative of it (FP16). Variant
 names may be given as substrings; default: every tiled variant that supports
 the shape. Correctness against the exact result is the tests' job; this tool
-only times the library.
+only times the library. --vendor adds the vendor library's GEMM on the same
+operands (FP16: torch.matmul, half output; INT8: torch._int_mm) to the
+rounds, as a yardstick for the same shapes; it is never part of the
+library's own path.
 """
 from __future__ import annotations
 
@@ -44,6 +47,7 @@ def main(argv=None) -> int:
     ap.add_argument("--variants", default="", help="comma-separated names or substrings")
     ap.add_argument("--rounds", type=int, default=5)
     ap.add_argument("--json", default="", help="write the results here")
+    ap.add_argument("--vendor", action="store_true", help="also time the vendor library (FP16, INT8)")
     ap.add_argument("--transposed-b", action="store_true",
                     help="also time mpgemm_gemm_bt (B stored K x N row-major) on the same operands "
                          "(FP16, INT8)")
@@ -82,10 +86,13 @@ def main(argv=None) -> int:
             if args.transposed_b and dt in ("f16", "s8"):
                 Bt = Bd.t().contiguous()  # the same B, K x N row-major
                 runs.append(("bt", None, "transposed B (mpgemm_gemm_bt)"))
+            if args.vendor and dt in ("f16", "s8"):
+                runs.append(("vendor", None, "vendor library (A x B^T)"))
             if not runs:
                 continue
             out_dt = torch.float32 if dt == "f16" else torch.int32
-            Cs = [torch.empty((M, N), dtype=out_dt, device="cuda") for _ in runs]
+            Cs = [torch.empty((M, N), dtype=torch.float16 if (r[0] == "vendor" and dt == "f16") else out_dt,
+                              device="cuda") for r in runs]
             reps = max(2, min(200, int(2e11 / (2 * M * N * K))))
             times = [[] for _ in runs]
 
@@ -93,6 +100,11 @@ def main(argv=None) -> int:
                 v, sp, _ = runs[i]
                 if v == "bt":
                     mp.gemm_bt(dt, Ad, Bt, C=Cs[i], stream=stream)
+                elif v == "vendor":
+                    if dt == "f16":
+                        torch.matmul(Ad, Bd.t(), out=Cs[i])
+                    else:
+                        torch._int_mm(Ad, Bd.t(), out=Cs[i])
                 else:
                     mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp)
 
@@ -115,16 +127,16 @@ def main(argv=None) -> int:
             for i, (v, sp, label) in enumerate(runs):
                 ms = float(np.median(times[i]))
                 tops = 2 * M * N * K / (ms * 1e-3) / 1e12
-                name = "transposed_b" if v == "bt" else mp.variant_name(dt, v)
+                name = {"bt": "transposed_b", "vendor": "vendor"}.get(v) if isinstance(v, str) else mp.variant_name(dt, v)
                 peak = PEAK_FP6 if name.startswith("fp6") else PEAK[dt]
                 if i == 0:
                     same = "ref"
                 elif dt == "f16":
-                    same = "close" if bool((Cs[i] - ref).abs().max() <= 1e-3 * ref.abs().max()) else "DIFFERENT"
+                    same = "close" if bool((Cs[i].float() - ref).abs().max() <= 1e-3 * ref.abs().max()) else "DIFFERENT"
                 else:
                     same = "identical" if torch.equal(Cs[i], ref) else "DIFFERENT"
                 spread = 100 * (max(times[i]) - min(times[i])) / ms
-                vtag = "bt" if v == "bt" else f"{v:2d}"
+                vtag = {"bt": "bt", "vendor": "vd"}.get(v) if isinstance(v, str) else f"{v:2d}"
                 print(f"{dt} {M}x{N}x{K} v{vtag} {label:44s} {ms * 1e3:9.1f} us {tops:8.1f} T/s "
                       f"{100 * tops / peak:5.1f}% of peak  rel {base / ms:5.3f}  spread {spread:4.1f}%  {same}",
                       flush=True)
