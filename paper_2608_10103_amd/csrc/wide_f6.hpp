@@ -7,10 +7,10 @@
 // MFMA, but the schedule of wide_gemm.hpp:
 //
 //  * 4 waves of 128 x 128 (4 x 4 blocks of 32 x 32, 256 FP32 accumulators
-//    per lane, all AGPRs). Operand bytes read from LDS per MFMA are half
-//    those of the 8-wave 128 x 64 layout; at the FP6 rate (a 32x32x64 MFMA
-//    every 32 cycles per SIMD) that layout asks the LDS for more bytes per
-//    cycle than it delivers.
+//    per lane, all AGPRs). Operand bytes read from LDS per MFMA are two
+//    thirds of those of the 8-wave 128 x 64 layout, which at the FP6 rate (a
+//    32x32x64 MFMA every 32 cycles per SIMD) asks the LDS for more bytes per
+//    cycle than its port delivers.
 //  * MFMAs as inline assembly with the accumulator tied to its AGPRs (left
 //    to the compiler, full AGPRs make it shuffle accumulators every
 //    iteration).
