@@ -6,8 +6,10 @@
 // bias 3, 2 mantissa bits: 0, 1, 2, 3, 4, 5, 6, 7 and 8 are all normal or
 // zero), each product of two is an integer of magnitude <= 64, and the FP32
 // accumulator holds every partial sum exactly while it stays <= 2^24, i.e.
-// for K <= 2^18. The result, converted to int32, is the exact INT4 GEMM of
-// the paper's Eq. (1) with INT32 accumulation (Section "INT4").
+// for K <= 2^18. The result, converted to int32, is the exact INT4 GEMM
+// D = A B (the paper's MMA primitive D = AB + C, Background, started from
+// zero) with the INT32 accumulation of its INT4 MMA (Listing
+// "lst:int4-primitives", part (c); Results and Analysis, Run 3).
 //
 // Two kernels:
 //  * s4_to_e3m2 converts each operand once (A: M rows, B: N columns, both

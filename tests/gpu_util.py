@@ -55,21 +55,27 @@ TORCH_OUT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
 
 def ulp_of(x, out):
-    """Spacing of the output format at |x| (the subnormal spacing below the
-    smallest normal)."""
+    """Spacing of the output format at |x|: 2^(e - fraction bits) for |x| in
+    [2^e, 2^(e+1)), the subnormal spacing below the smallest normal. The
+    binade comes from frexp (exact), not from a rounded log2."""
     frac, emin = _FORMATS[out]
     ax = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), 2.0 ** emin)
-    return np.ldexp(1.0, (np.floor(np.log2(ax)).astype(np.int64) - frac))
+    _, e = np.frexp(ax)  # ax = m 2^e, 0.5 <= m < 1: the binade starts at 2^(e - 1)
+    return np.ldexp(1.0, e.astype(np.int64) - 1 - frac)
 
 
 def assert_scaled(got, exact, D, out, what=""):
-    """Scaled outputs: the GPU scales in binary32 (at most 3 roundings before
-    the output rounding), so a result may sit one output ulp from the
-    correctly rounded value: |got - exact| <= 1 ulp (binary32 output: 4 ulp).
-    FP16 inputs add the sum's bound 1e-3 * D (D already scaled)."""
+    """Scaled outputs. Integer inputs: the exact sum is rounded to binary32,
+    multiplied by sa then sb in binary32 (three roundings, relative error
+    below 3 * 2^-24, i.e. under 3 binary32 ulp of the exact value), then
+    rounded to the output type: |got - exact| <= 3 ulp for binary32 output,
+    <= 1 ulp for binary16 / bfloat16 (half an ulp from the last rounding plus
+    the binary32 error, far below the other half). FP16 inputs add the sum's
+    bound 1e-3 * D (D already scaled) and 2^-21 |exact| for the binary32
+    scaling."""
     g = got.float().cpu().numpy().astype(np.float64)
     assert np.all(np.isfinite(g)), f"{what}: non-finite output"
-    tol = ulp_of(exact, out) * (4.0 if out == "f32" else 1.0)
+    tol = ulp_of(exact, out) * (3.0 if out == "f32" else 1.0)
     if D is not None:
         tol = tol + F16_TOL * D + 2.0 ** -21 * np.abs(exact)
     err = np.abs(g - exact)

@@ -81,8 +81,8 @@ def _swz(ch, q):
 
 # Swizzles of 64-byte rows, ((q >> a) ^ (q >> b)) & 3, that read at the rate
 # of the conflict-free 128-byte layout (within 3%) under the MFMA operand-read
-# pattern, measured on MI355X with paper_2608_10103_amd.probes.lds_probe
-# (profiles/lds_probe.md). A 16-lane bank model does not predict them: it
+# pattern, measured on MI355X with an LDS micro-benchmark (eight 1 KiB
+# ds_read_b128 per wave and iteration, 8 waves per CU). A 16-lane bank model does not predict them: it
 # calls ((q >> 1) ^ (q >> 3)) & 3 conflict-free, which measured 1.75x slower.
 MEASURED_FAST_64B = {(3, 7), (3, 4), (2, 5), (2, None), (3, 6), (3, 5), (2, 7), (2, 3), (2, 6),
                      (3, None), (1, 4), (0, 2), (1, 2), (0, 3)}
