@@ -11,14 +11,18 @@ Ops per GEMM are 2*N^3 (the paper's convention: its Table II TOPS column is
 
 Printed: one JSON line on stdout (progress goes to stderr) with
   value      whole-step throughput, total ops / wall time per step (TOP/s);
-  points     per-GEMM mean duration (HIP events on the launch stream, over the
-             timed region), TOP/s and fraction of the precision's dense MFMA
-             peak;
+  points     per-GEMM median duration (HIP events on the launch stream, over
+             the timed region; mean, min and max beside it), TOP/s and
+             fraction of the precision's dense MFMA peak, and the oracle's
+             check of sampled output rows (max FP16 normalised error, or
+             bit-exactness);
   roofline   the dominant kernel (largest share of step time) against its
              precision's MFMA peak, with HBM traffic from the committed
              counter profile when it still matches the kernel sources;
   cpu_baseline  the CPU oracle timed on this host on a bounded row sample of
-             the N = 8192 points, which also checks those GPU rows.
+             the N = 8192 points, which also checks those GPU rows;
+  clock_mhz  the shader clock sampled from the driver during the timed
+             region (null where the driver does not expose it).
 """
 from __future__ import annotations
 
@@ -43,7 +47,7 @@ PEAK_FP6 = 10100.0
 
 
 def point_peak(dtype: str, variant_name: str) -> float:
-    return PEAK_FP6 if variant_name.startswith("fp6") else PEAK[dtype]
+    return PEAK_FP6 if variant_name.startswith(("fp6", "e2m3")) else PEAK[dtype]
 PEAK_UNIT = {"f16": "TFLOP/s", "s8": "TOP/s", "s4": "TOP/s"}
 IN_BYTES = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 METRIC = "TFLOP/s | TOP/s at N=512–8192 for FP16, INT8, INT4; % of MFMA peak per dtype"
@@ -71,7 +75,8 @@ KERNEL_SOURCES = {"generic": ["generic_gemm.hpp"], "tile": ["tiled_gemm.hpp"], "
                   "pingpong": ["tiled_gemm.hpp"], "fp6pipe": ["tiled_gemm.hpp", "f6_gemm.hpp"],
                   "deep": ["tiled_gemm.hpp", "deep_gemm.hpp"], "skinny": ["skinny_gemm.hpp"],
                   "wide": ["tiled_gemm.hpp", "wide_gemm.hpp"],
-                  "fp6wide": ["tiled_gemm.hpp", "f6_gemm.hpp", "wide_gemm.hpp", "wide_f6.hpp"]}
+                  "fp6wide": ["tiled_gemm.hpp", "f6_gemm.hpp", "wide_gemm.hpp", "wide_f6.hpp"],
+                  "e2m3wide": ["tiled_gemm.hpp", "f6_gemm.hpp", "wide_gemm.hpp", "wide_i4.hpp"]}
 
 
 def kernel_source_hash(variant_name: str) -> str:
@@ -168,8 +173,12 @@ def main():
         v = forced.get((dt, n))
         vsel = v if v is not None else mp.select_variant(dt, n, n, n, Ad.data_ptr(), Bd.data_ptr(),
                                                          C.data_ptr())
+        # the default choice needs no workspace; a forced variant may (split K,
+        # FP6 pre-pass): allocated here, before timing
+        wsb = mp.workspace_size(dt, n, n, n, variant=v)
+        ws = mp.new_workspace(wsb, dev) if wsb else None
         bufs.append(dict(dt=dt, n=n, seed=seed, A=Ad, B=Bd, C=C, host=(A, B), variant=v,
-                         vname=mp.variant_name(dt, vsel)))
+                         vname=mp.variant_name(dt, vsel), ws=ws, ws_bytes=wsb))
     torch.cuda.synchronize()
 
     stream = torch.cuda.Stream(device=dev)  # default priority
@@ -179,7 +188,7 @@ def main():
         for i, b in enumerate(bufs):
             if events is not None:
                 events[i][0].record(stream)
-            fns[b["dt"]](b["A"], b["B"], C=b["C"], stream=stream, variant=b["variant"])
+            fns[b["dt"]](b["A"], b["B"], C=b["C"], stream=stream, variant=b["variant"], workspace=b["ws"])
             if events is not None:
                 events[i][1].record(stream)
 
@@ -192,13 +201,16 @@ def main():
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             for _ in bufs] for _ in range(args.steps)]
     log(f"timing {args.steps} steps")
+    clock = ClockSampler()
     torch.cuda.synchronize()
+    clock.start()
     t0 = time.perf_counter()
     with torch.cuda.stream(stream):
         for s in range(args.steps):
             step(evs[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    clock_mhz = clock.stop()
     log(f"timed region {wall * 1e3:.1f} ms")
 
     ms_per_step = wall * 1e3 / args.steps
@@ -208,11 +220,12 @@ def main():
     pts = []
     for i, b in enumerate(bufs):
         ms = [evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)]
-        mean_ms = float(np.mean(ms))
+        med_ms, mean_ms = float(np.median(ms)), float(np.mean(ms))
         ops = gemm_ops(b["n"], b["n"], b["n"])
-        tops = ops / (mean_ms * 1e-3) / 1e12
-        pts.append(dict(dtype=b["dt"], n=b["n"], variant=b["vname"], ms=round(mean_ms, 5),
-                        ms_min=round(float(np.min(ms)), 5), ms_max=round(float(np.max(ms)), 5),
+        tops = ops / (med_ms * 1e-3) / 1e12
+        pts.append(dict(dtype=b["dt"], n=b["n"], variant=b["vname"], ms=round(med_ms, 5),
+                        ms_mean=round(mean_ms, 5), ms_min=round(float(np.min(ms)), 5),
+                        ms_max=round(float(np.max(ms)), 5),
                         tops=round(tops, 2), frac_peak=round(tops / point_peak(b["dt"], b["vname"]), 4),
                         total_ms=mean_ms * args.steps))
 
@@ -241,6 +254,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(bufs, log)
+        for p, chk in zip(pts, cpu.pop("point_checks")):
+            p["check"] = chk
 
     out = {
         "metric": METRIC,
@@ -261,13 +276,66 @@ def main():
                         if args.points == "sweep" else f"points {args.points}",
             "points": len(bufs),
             "ops_per_step": total_ops,
+            "entry_points": "gemm_f16_f32, gemm_s8_s32, gemm_s4_s32 (no workspace)"
+                            if not forced else "forced variants via mpgemm_run_variant(_ws)",
+            "workspace_bytes": int(sum(b["ws_bytes"] for b in bufs)),
         },
+        "clock_mhz": clock_mhz,
         "device": {"name": props.name, "cus": props.multi_processor_count},
         "points": pts,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+class ClockSampler:
+    """Samples the GPU shader clock the driver reports (the active level of
+    pp_dpm_sclk in sysfs) every 20 ms on a host thread; stop() returns the
+    median, min and max in MHz, or None where the file is not readable."""
+
+    def __init__(self):
+        import glob
+        self.files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.samples = []
+        self._run = False
+        self._t = None
+
+    def _read(self):
+        for f in self.files:
+            try:
+                for line in open(f):
+                    if line.rstrip().endswith("*"):
+                        return float(line.split(":")[1].strip().rstrip("*").strip().lower().rstrip("mhz"))
+            except (OSError, ValueError, IndexError):
+                continue
+        return None
+
+    def _loop(self):
+        while self._run:
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+            time.sleep(0.02)
+
+    def start(self):
+        import threading
+        if not self.files or self._read() is None:
+            return
+        self._run = True
+        self._t = threading.Thread(target=self._loop, daemon=True)
+        self._t.start()
+
+    def stop(self):
+        if self._t is None:
+            return None
+        self._run = False
+        self._t.join()
+        if not self.samples:
+            return None
+        return {"median": float(np.median(self.samples)), "min": float(np.min(self.samples)),
+                "max": float(np.max(self.samples)), "samples": len(self.samples),
+                "source": "pp_dpm_sclk active level"}
 
 
 def _read_counter(folder, counter, name_filter):
@@ -351,6 +419,21 @@ def cpu_baseline(bufs, log):
             ok = bool(np.array_equal(got.astype(np.int64), ref))
         checked = checked and ok
         parts.append(f"{dt} N={n}: {len(rows)} rows in {dt_s:.2f} s")
+    # every point: the oracle on 8 sampled rows (plus the first and the last),
+    # max FP16 normalised error or bit-exactness of those GPU rows
+    checks = []
+    for b in bufs:
+        dt, n = b["dt"], b["n"]
+        rows = si.sample_rows(b["seed"] + 3000, n, min(8, n), force=(0, n - 1))
+        A, B = b["host"]
+        got = b["C"][torch.from_numpy(rows.astype(np.int64)).to(b["C"].device)].cpu().numpy()
+        if dt == "f16":
+            ref, D = oracle.gemm_f16(A, B, rows=rows, threads=threads)
+            checks.append({"rows": int(len(rows)), "max_norm_err": float(oracle.normalized_error(got, ref, D))})
+        else:
+            ref = oracle.gemm_s8(A, B, rows=rows, threads=threads) if dt == "s8" else \
+                oracle.gemm_s4(A, B, rows=rows, threads=threads)
+            checks.append({"rows": int(len(rows)), "bit_exact": bool(np.array_equal(got.astype(np.int64), ref))})
     try:
         model = next(l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo")
                      if l.startswith("model name"))
@@ -364,7 +447,9 @@ def cpu_baseline(bufs, log):
         "sample": "; ".join(parts) + " (2*rows*N*N ops each)",
         "cpu_model": model,
         "cpu_count": os.cpu_count(),
-        "gpu_rows_match_oracle": checked,
+        "gpu_rows_match_oracle": checked and all(c.get("bit_exact", True) and c.get("max_norm_err", 0.0) <= 1e-3
+                                                 for c in checks),
+        "point_checks": checks,
     }
 
 

@@ -19,21 +19,16 @@
  *   C  row-major M x N:     C[i][j] at element i*N + j.
  *
  * Memory and ownership. A, B and C are DEVICE pointers on the current HIP
- * device, owned by the caller; the library never allocates, frees or copies
- * them and keeps no pointer after the call returns. C must not overlap A or B.
- * Any alignment is accepted; operands whose shapes and alignment suit a tuned
- * tile take the fast kernels, everything else a bounds-checked kernel.
- * Workspace: the INT4 kernels on the FP6 matrix cores first convert A and B
- * into a device workspace of 24 * (ceil(M/256) + ceil(N/256)) * 256 *
- * ceil(K/256) * 8 bytes (0.75 byte per padded element). The library keeps
- * one such buffer per (device, stream) pair (hipStreamPerThread: per host
- * thread): allocated with hipMalloc on the stream's first such call, grown
- * when a larger problem arrives (that call first synchronises the stream,
- * whose earlier calls may still read the old buffer), and held until the
- * process ends. Calls on one stream reuse it in stream order; calls on
- * different streams never share one. A stream handle that is destroyed while
- * INT4 work is still pending on it must not be reused by a new stream for
- * INT4 calls before that work has finished.
+ * device, owned by the caller; the library never allocates, frees, copies or
+ * synchronises, keeps no pointer after the call returns and holds no state
+ * between calls. C must not overlap A or B. Any alignment is accepted;
+ * operands whose shapes and alignment suit a tuned tile take the fast
+ * kernels, everything else a bounds-checked kernel.
+ * Scratch memory: the plain entry points (gemm_f16_f32, gemm_s8_s32,
+ * gemm_s4_s32, gemm_scaled) use none; they only choose kernels that need no
+ * scratch. Split K, the INT4 kernels fed by an FP6 conversion pre-pass and
+ * zero points take scratch from a caller-owned workspace passed to
+ * mpgemm_gemm_ws / mpgemm_run_variant_ws (see "workspace" below).
  *
  * Streams. Work is enqueued on `stream` (0 = the null stream), which must
  * belong to the current device, and the call returns without synchronising.
@@ -46,9 +41,6 @@
  *                         pointer NULL (A and B when M, N, K > 0; C when
  *                         M, N > 0); C overlapping A or B; a problem whose
  *                         element counts overflow 64-bit byte offsets;
- *   hipErrorOutOfMemory   a workspace (INT4 on the FP6 cores; split K, see
- *                         mpgemm_select_splits) could not be allocated, or
- *                         the error of synchronising the stream to grow it;
  *   the launch error      if a kernel launch itself fails.
  * Nothing is enqueued when an argument error is returned.
  * Degenerate sizes: M == 0 or N == 0 is a no-op returning hipSuccess; K == 0
@@ -85,10 +77,13 @@ hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, in
  * two's-complement nibbles packed two per byte along K, the low nibble holding
  * the even k: A is M rows of K/2 bytes, B is N rows of K/2 bytes. Exact
  * whenever every partial sum fits in int32, which always holds for K < 2^25
- * (|a*b| <= 64). gfx950 has no 4-bit integer MFMA: for K <= 2^18 the values
- * are converted to FP6 E3M2 (which represents -8..8 exactly) and multiplied
- * on the FP6 MFMA, whose FP32 accumulation is exact below 2^24; other
- * problems run on the INT8 MFMA or the bounds-checked kernel. */
+ * (|a*b| <= 64). gfx950 has no 4-bit integer MFMA: for K a multiple of 256
+ * up to 65536 the kernel feeds each value v as the FP6 E2M3 code v + 8
+ * (value (v + 8) / 8, exact) to the FP6 MFMA, converting inside the GEMM,
+ * and removes the bias with row and column sums it takes on the way; every
+ * FP32 partial sum is then a multiple of 1/64 below 2^18, held exactly.
+ * Other problems run on the INT8 MFMA (K < 131072) or the bounds-checked
+ * kernel. */
 hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
                        hipStream_t stream);
 
@@ -106,16 +101,18 @@ hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, 
  * sums of A and column sums of B), converted to binary32 once, multiplied by
  * sa[i] then sb[j] in binary32, and rounded to nearest even into the output
  * type; so the result is within 1 unit in the last place of the output type
- * of the exactly rounded value (binary32 output: within 3 ulp). FP16 inputs:
+ * of the exact value (binary32 output: within 3 ulp). FP16 inputs:
  * the binary32 sum of the plain entry point (same error bound), scaled the
  * same way; zero points are not accepted. The struct is a HOST pointer read
  * during the call; the vectors it points to are DEVICE arrays of M (for _a)
  * or N (for _b) elements, 4-byte aligned. C holds M x N elements of the
  * output type, row-major (2-byte aligned for FP16/BF16, 4-byte for FP32).
- * Zero points cost one extra pass over A and/or B (row sums, kept in the
- * per-stream workspace: 4 (M + N) bytes). Errors as for the plain entry
- * points, plus hipErrorInvalidValue for a NULL struct, an unknown output
- * type, zero points with FP16 inputs or misaligned vectors. */
+ * Zero points cost one extra pass over A and/or B (row sums, kept in a
+ * workspace): gemm_scaled takes no workspace and refuses zero points; pass
+ * them to mpgemm_gemm_ws. Errors as for the plain entry points, plus
+ * hipErrorInvalidValue for a NULL struct, an unknown output type, zero
+ * points (here) or zero points with FP16 inputs (everywhere), misaligned
+ * vectors. */
 enum { MPGEMM_OUT_F32 = 1, MPGEMM_OUT_F16 = 2, MPGEMM_OUT_BF16 = 3 };
 
 typedef struct mpgemm_epilogue {
@@ -130,6 +127,49 @@ typedef struct mpgemm_epilogue {
  * plain entry points); C receives the scaled output. */
 hipError_t gemm_scaled(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
                        const mpgemm_epilogue *epi, hipStream_t stream);
+
+/* ---- workspace: scratch memory owned by the caller ----
+ * Some kernels need device scratch memory besides A, B and C: split K (the
+ * partial tiles of the K ranges and one counter per tile; the automatic
+ * choice splits only skinny problems, see mpgemm_select_splits), the INT4
+ * kernels fed by an FP6 conversion pre-pass (the converted operands, 0.75
+ * byte per padded element) and zero points (row sums of A and column sums
+ * of B). The library never allocates it: the caller passes a workspace.
+ *
+ * mpgemm_workspace_size: bytes of workspace the call with the same arguments
+ * would use, into *bytes (0: none). variant < 0 and splits == 0 ask for the
+ * automatic choice made with a large enough workspace; epi may be NULL.
+ * Returns hipErrorInvalidValue for arguments the call would refuse (sizes,
+ * epilogue, a variant that cannot run the problem, a bad split count).
+ *
+ * mpgemm_gemm_ws: the operation of the dtype's entry point (dtype 0 = FP16
+ * -> FP32, 1 = INT8 -> INT32, 2 = INT4 -> INT32), with scaled outputs when
+ * epi is not NULL (as gemm_scaled, zero points allowed), using `workspace`
+ * (DEVICE memory on the current device, 256-byte aligned, not overlapping A,
+ * B or C, `workspace_bytes` long) for scratch. With workspace == NULL or
+ * workspace_bytes == 0 it is the plain entry point (or gemm_scaled); a
+ * workspace smaller than the automatic choice wants makes it choose a kernel
+ * that needs less (no split), except that zero points always need theirs.
+ * Contract:
+ *   - zero-fill the workspace once before its first use (hipMemset after
+ *     allocating it); every completed call leaves the counter block (the
+ *     first 64 KiB) zero again, so later calls need no clearing;
+ *   - one call at a time per workspace: calls that may run concurrently
+ *     (other streams, other threads) need workspaces of their own; calls in
+ *     order on one stream may share one;
+ *   - the library keeps no pointer to it after the call returns; free it
+ *     once the stream's pending work that uses it has completed.
+ * Errors: those of the entry points, plus hipErrorInvalidValue for a
+ * misaligned or overlapping workspace, or one too small for the scratch the
+ * call cannot do without (zero points; an explicit split or FP6 pre-pass
+ * variant in mpgemm_run_variant_ws). Nothing is enqueued then. */
+hipError_t mpgemm_workspace_size(int dtype, int variant, int splits, int M, int N, int K,
+                                 const mpgemm_epilogue *epi, size_t *bytes);
+
+hipError_t mpgemm_gemm_ws(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                          const mpgemm_epilogue *epi, void *workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
 
 /* B stored K x N ROW-major (B(k,j) at element k*N + j, N-contiguous): the
  * "transposed B" operand layout of the paper's INT4 ablation (Table XII),
@@ -177,29 +217,27 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
  * finish adds the ranges' partial sums in range order 0, 1, ... and writes C,
  * so results do not depend on scheduling (FP16: the summation order differs
  * from the unsplit kernel's, within the same error bound; integers: exact).
- * Partials and per-tile counters live in a per-(device, stream) workspace
- * like the FP6 one (allocated on first use, grown after synchronising the
- * stream, counters zeroed on the stream when allocated, kept until the
- * process ends). The entry points split only problems with a small side:
+ * Partials and per-tile counters live in the caller's workspace. With a
+ * workspace, the automatic choice splits only problems with a small side:
  * the narrow tiles (at most 256 rows on one side, at least 1024 on the other)
  * while the grid stays within 128 workgroups, up to 4 ranges; where those do
  * not apply, the 128x128 tiles of problems with M or N at most 128 up to 256
  * workgroups, 4 ranges for FP16, 2 for the integer types. */
 
-/* Splits the entry points use for this variant and problem (1 = none), or -1
- * for an invalid dtype, variant or size. */
+/* Splits the automatic choice uses for this variant and problem when a large
+ * enough workspace is given (1 = none), or -1 for an invalid dtype, variant
+ * or size. */
 int mpgemm_select_splits(int dtype, int variant, int M, int N, int K);
 
-/* mpgemm_run_variant with an explicit split count; hipErrorInvalidValue also
- * when the variant cannot split (only the pipelined ones can), splits < 1 or
- * > 16, or K's slices do not divide evenly into `splits`. */
-hipError_t mpgemm_run_variant_splits(int dtype, int variant, int splits, int M, int N, int K,
-                                     const void *A, const void *B, void *C, hipStream_t stream);
-
-/* gemm_scaled with an explicit variant and split count (0 = automatic). */
-hipError_t mpgemm_run_variant_scaled(int dtype, int variant, int splits, int M, int N, int K,
-                                     const void *A, const void *B, void *C,
-                                     const mpgemm_epilogue *epi, hipStream_t stream);
+/* One specific variant with an explicit split count (0 = the automatic
+ * choice for the variant), scaled outputs when epi is not NULL, and a
+ * workspace as for mpgemm_gemm_ws. hipErrorInvalidValue also when the
+ * variant cannot run the problem, splits > 1 for a variant that cannot
+ * split, splits > 16, K's slices not dividing evenly into `splits`, or the
+ * workspace too small for the split or the FP6 pre-pass the variant needs. */
+hipError_t mpgemm_run_variant_ws(int dtype, int variant, int splits, int M, int N, int K, const void *A,
+                                 const void *B, void *C, const mpgemm_epilogue *epi, void *workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
 
 /* Host-side view of the INT4 -> FP6 conversion the FP6 kernels apply on the
  * device (same source): `in` is one run of 16 HOST bytes = 32 nibbles, word
@@ -209,6 +247,18 @@ hipError_t mpgemm_run_variant_scaled(int dtype, int variant, int splits, int M, 
  * word d, low nibble for h = 0, high nibble for h = 1 (i.e. k offset
  * 8d + 2i + h). For tests of the encoding; never touches the GPU. */
 void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out);
+
+/* Host-side view of the conversion the INT4 kernel with the conversion
+ * inside the GEMM applies on the device (same source): `in` is one run of 16
+ * HOST bytes = 32 nibbles (word d = bytes 4d..4d+3, little-endian); `out` (6
+ * words, HOST) receives 32 six-bit FP6 E2M3 codes, field f at bits
+ * [6f, 6f+6) of the 192-bit little-endian string. The code of a nibble v is
+ * v + 8 (the nibble with its top bit flipped), value (v + 8) / 8. Input
+ * words (x, y) = (word 2p, word 2p + 1) fill fields 16p .. 16p + 15 with
+ * their nibbles (nibble n of a word at bits 4n..4n+3) in the order
+ * x0 y1 x3 y4 x6 y7 x1 y2 x4 y5 x7 y0 x2 y3 x5 y6. For tests of the
+ * encoding; never touches the GPU. */
+void mpgemm_s4_run_to_e2m3(const uint8_t *in, uint32_t *out);
 
 #ifdef __cplusplus
 }

@@ -3,18 +3,13 @@
 // Every entry point validates its arguments on the host, picks a kernel
 // variant (a tiled kernel when the problem fits its constraints, the
 // bounds-checked kernel otherwise) and launches it on the caller's stream with
-// hipLaunchKernel, returning the launch status. Nothing here copies or
-// synchronises, except that the INT4 variants on the FP6 matrix cores keep a
-// workspace for the converted operands per (device, stream), allocated on
-// first use and grown (after synchronising that stream) when a larger problem
-// arrives.
+// hipLaunchKernel, returning the launch status. Nothing here allocates,
+// frees, copies or synchronises, and no state is kept between calls: the
+// kernels that need scratch memory (split K, the FP6 pre-pass variants, the
+// zero-point row sums) take it from a workspace the caller passes in.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
-
-#include <mutex>
-#include <thread>
-#include <vector>
 
 #include "mpgemm.h"
 #include "variants.hpp"
@@ -118,6 +113,12 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
                                                                                           : F6Geom::rows_pad(N)) <= INT_MAX;
         return true;
     }
+    if (v.kind == I4WIDE) {
+        // whole 256-k slice pairs, K within the exact range of the biased
+        // E2M3 sums, 16-byte aligned rows; M and N may be ragged
+        if (dtype != S4 || K % v.bkb || K > WideI4Cfg::MAX_K) return false;
+        return aligned(A, 16) && aligned(B, 16);
+    }
     const long kb = row_bytes(dtype, K);
     // edge tiles are predicated in M and N; K must fill whole slices
     if (kb % v.bkb) return false;
@@ -190,20 +191,18 @@ enum : int {
     V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
 };
 // INT4-only variants follow the common list in kS4.
-constexpr int V_FP6_256_S2 = kNumF16 + 1;  // fp6pipe256x256_w2x4_k128_s2
-constexpr int V_FP6_WIDE = kNumF16 + 8;    // fp6wide256x256_w2x2_k128_s3
+constexpr int V_I4WIDE = kNumCommon + 9;   // e2m3wide256x256_w2x2_k256
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
 // taken when it supports the problem and yields at least `min_tiles`
 // workgroups (256 = one per CU). Chosen from interleaved timings of every
 // variant at N = 512 ... 8192 on MI355X.
 struct Pref { int variant; long min_tiles; };
-// INT4: the one-wave-per-SIMD FP6 kernel once 256 x 256 tiles fill the CUs
-// (1.10x the INT8-MFMA kernel at 4096^3 with the conversion counted, 1.14-
-// 1.19x the 8-wave FP6 kernel at 4096..16384 x 8192 x 2048..16384; below
-// 256 tiles the conversion does not pay off), the 8-wave FP6 kernel where
-// the first's 32-bit workspace offsets do not reach, then the INT8-MFMA
-// kernels.
+// INT4: the FP6 kernel with the conversion inside the GEMM (no pre-pass, no
+// workspace) from 64 tiles of 256 x 256 (N = 2048 square); below that, or
+// for K beyond its exact range or off its 256-k grid, the INT8-MFMA kernels.
+// The FP6 kernels fed by a conversion pre-pass need a workspace and are
+// never chosen automatically.
 // FP16, INT8: below 256 tiles of 256 x 256 the 128-byte-slice 128 x 128
 // kernel (as fast or faster than the 64-byte one at every measured size:
 // square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
@@ -214,8 +213,8 @@ struct Pref { int variant; long min_tiles; };
 // predicated edges, where M or N is not a multiple of 256.
 const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_FP6_WIDE, 256}, {V_FP6_256_S2, 512}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256},
-                        {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS4[] = {{V_I4WIDE, 64}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1},
+                        {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the
 // narrow tiles below (measured on MI355X at 1..32 x {4096, 8192, 14336,
@@ -318,93 +317,42 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     return 0;
 }
 
-// Workspaces: one device buffer per (device, stream, purpose) triple, so
-// calls on one stream reuse it in stream order and calls on different
-// streams never share one. Purposes: the FP6 operand copies, the split-K
-// counters + partials, and the row sums the zero-point epilogue needs. A buffer grows when a larger problem arrives: the
-// stream is synchronised first (earlier calls on it may still use the old
-// buffer), then the old buffer is freed and a larger one allocated; a new
-// split-K buffer has its counter block zeroed on the stream (a fill kernel,
-// no memset). Buffers are kept until the process ends. hipStreamPerThread
-// names a different stream in every host thread, so it is keyed by thread
-// as well.
-enum Slot { SLOT_FP6 = 0, SLOT_SPLITK = 1, SLOT_SUMS = 2 };
+// Caller workspace. Layout: [0, 64 KiB) the split-K tile counters (zero
+// before the first split call on a workspace; every split call leaves the
+// counters it used zero again), then the zero-point row sums (4 (M + N)
+// bytes), then the split-K partial tiles or the FP6 operand copies; every
+// part 256-byte aligned. A problem that needs no scratch needs no workspace.
+constexpr size_t kWsAlign = 256;
 
-__global__ void zero_words(uint32_t *p, int n) {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
-}
+size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
-struct Workspace {
-    int dev;
-    hipStream_t stream;
-    std::thread::id thread;
-    int slot;
-    void *ptr;
-    size_t bytes;
+struct WsPlan {
+    size_t sums_off, data_off, total;  // total 0: no workspace needed
 };
 
-hipError_t stream_workspace(hipStream_t stream, int slot, size_t bytes, void **out) {
-    static std::mutex mu;
-    static std::vector<Workspace> spaces;
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    const std::thread::id tid =
-        stream == hipStreamPerThread ? std::this_thread::get_id() : std::thread::id();
-    std::lock_guard<std::mutex> lock(mu);
-    Workspace *w = nullptr;
-    for (Workspace &s : spaces)
-        if (s.dev == dev && s.stream == stream && s.thread == tid && s.slot == slot) w = &s;
-    if (w && w->bytes >= bytes) {
-        *out = w->ptr;
-        return hipSuccess;
-    }
-    if (w) {
-        e = hipStreamSynchronize(stream);
-        if (e != hipSuccess) return e;
-        e = hipFree(w->ptr);
-        w->ptr = nullptr;
-        w->bytes = 0;
-        if (e != hipSuccess) return e;
-    }
-    const size_t granule = (size_t)2 << 20;
-    const size_t want = (bytes + granule - 1) / granule * granule;
-    void *p = nullptr;
-    e = hipMalloc(&p, want);
-    if (e != hipSuccess) return e;
-    if (slot == SLOT_SPLITK) {
-        uint32_t *words = static_cast<uint32_t *>(p);
-        int n = kSplitCounters;
-        void *args[] = {&words, &n};
-        e = hipLaunchKernel(reinterpret_cast<const void *>(&zero_words), dim3(64), dim3(256), args, 0,
-                            stream);
-        if (e != hipSuccess) {
-            (void)hipFree(p);
-            return e;
-        }
-    }
-    if (!w) {
-        spaces.push_back(Workspace{dev, stream, tid, slot, nullptr, 0});
-        w = &spaces.back();
-    }
-    w->ptr = p;
-    w->bytes = want;
-    *out = p;
-    return hipSuccess;
+WsPlan ws_plan(const Variant &v, int splits, int M, int N, int K, bool zero_points) {
+    const size_t sums = zero_points ? align_up(((size_t)M + N) * 4) : 0;
+    size_t data = 0;
+    if (splits > 1) data = (size_t)tile_count(v, M, N) * splits * v.bm * v.bn * 4;
+    else if (v.kind == FP6 || v.kind == FP6WIDE) data = F6Geom::bytes(M, K) + F6Geom::bytes(N, K);
+    if (!sums && !data) return WsPlan{0, 0, 0};
+    return WsPlan{kSplitCounterBytes, kSplitCounterBytes + sums, kSplitCounterBytes + sums + data};
 }
 
-// INT4 on the FP6 matrix cores: convert both operands into the stream's
-// workspace, then run the FP6 tile kernel.
+struct Ws {
+    uint8_t *p;    // caller's device workspace, or null
+    size_t bytes;  // its size (0 without one)
+};
+
+// INT4 on the FP6 matrix cores fed by the conversion pre-pass: convert both
+// operands into the workspace, then run the FP6 tile kernel.
 hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, const uint8_t *B,
-                      void *C, EpiParams epi, hipStream_t stream) {
+                      void *C, EpiParams epi, uint8_t *w, hipStream_t stream) {
     const long Ma = F6Geom::rows_pad(M), Nb = F6Geom::rows_pad(N), runs = F6Geom::runs_pad(K);
-    const uint64_t a_bytes = F6Geom::bytes(M, K), b_bytes = F6Geom::bytes(N, K);
-    void *ws = nullptr;
-    hipError_t e = stream_workspace(stream, SLOT_FP6, a_bytes + b_bytes, &ws);
-    if (e != hipSuccess) return e;
-    uint8_t *w = static_cast<uint8_t *>(ws);
+    const uint64_t a_bytes = F6Geom::bytes(M, K);
     F6Prep pa{A, w, w + (size_t)Ma * runs * 16, M, (int)Ma, K, (int)runs};
     F6Prep pb{B, w + a_bytes, w + a_bytes + (size_t)Nb * runs * 16, N, (int)Nb, K, (int)runs};
+    hipError_t e;
     {
         void *args[] = {&pa, &pb};
         dim3 grid((unsigned)((runs + F6_PREP_RUNS - 1) / F6_PREP_RUNS),
@@ -419,8 +367,7 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
         // the one-wave-per-SIMD kernel's table entry stores raw sums of whole
         // tiles; ragged or scaled outputs take its shared-epilogue instantiation
         const void *fn = v.fn;
-        if (v.kind == FP6WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn))
-            fn = reinterpret_cast<const void *>(&wide_f6_gemm<false>);
+        if (v.kind == FP6WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) fn = v.fn_epi;
         void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &epi};
         e = hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
@@ -428,10 +375,10 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
 }
 
 hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, const void *A,
-                  const void *B, void *C, EpiParams epi, hipStream_t stream) {
+                  const void *B, void *C, EpiParams epi, const WsPlan &plan, Ws ws, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
-    if (v.kind == FP6 || v.kind == FP6WIDE) return launch_fp6(v, M, N, K, a, b, C, epi, stream);
+    if (v.kind == FP6 || v.kind == FP6WIDE) return launch_fp6(v, M, N, K, a, b, C, epi, ws.p + plan.data_off, stream);
     if (v.kind == SKINNY) {
         // X = the operand with at most bm rows (A when M is small), W = the other
         int trans = M <= v.bm ? 0 : 1;
@@ -450,36 +397,28 @@ hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, 
     int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
     if (!v.splitk) {
         const void *fn = v.fn;
-        // the one-wave-per-SIMD kernel's table entry stores raw sums; scaled
-        // outputs take its instantiation with the shared epilogue
-        if (v.kind == WIDE && epi.out != OUT_PLAIN)
-            fn = dtype == F16 ? reinterpret_cast<const void *>(&wide_gemm<F16, false>)
-                              : reinterpret_cast<const void *>(&wide_gemm<S8, false>);
+        // the one-wave-per-SIMD kernels' table entries store raw sums of whole
+        // tiles; scaled outputs (and for INT4 ragged edges) take their
+        // instantiation with the shared epilogue
+        if (v.kind == WIDE && epi.out != OUT_PLAIN) fn = v.fn_epi;
+        if (v.kind == I4WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) fn = v.fn_epi;
         void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &epi};
         return hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
     }
     int *counters = nullptr;
     uint32_t *partials = nullptr;
     if (splits > 1) {
-        const size_t part_bytes = (size_t)tiles_m * tiles_n * splits * v.bm * v.bn * 4;
-        void *ws = nullptr;
-        hipError_t e = stream_workspace(stream, SLOT_SPLITK, kSplitCounterBytes + part_bytes, &ws);
-        if (e != hipSuccess) return e;
-        counters = static_cast<int *>(ws);
-        partials = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(ws) + kSplitCounterBytes);
+        counters = reinterpret_cast<int *>(ws.p);
+        partials = reinterpret_cast<uint32_t *>(ws.p + plan.data_off);
     }
     void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &splits, &counters, &partials, &epi};
     return hipLaunchKernel(v.fn, dim3(tiles_m * tiles_n * splits), dim3(v.threads), args, 0, stream);
 }
 
-// Row sums for the zero-point terms into the stream's sums workspace.
+// Row sums for the zero-point terms into the workspace's sums part.
 hipError_t zero_point_sums(int dtype, int M, int N, int K, const void *A, const void *B,
-                           EpiParams &epi, hipStream_t stream) {
+                           EpiParams &epi, int *sums, hipStream_t stream) {
     if (!epi.zero_a && !epi.zero_b) return hipSuccess;
-    void *ws = nullptr;
-    hipError_t e = stream_workspace(stream, SLOT_SUMS, ((size_t)M + N) * 4, &ws);
-    if (e != hipSuccess) return e;
-    int *sums = static_cast<int *>(ws);
     const void *fn = dtype == S8 ? reinterpret_cast<const void *>(&row_sums<S8>)
                                  : reinterpret_cast<const void *>(&row_sums<S4>);
     if (epi.zero_b) {  // needs the row sums of A
@@ -487,7 +426,7 @@ hipError_t zero_point_sums(int dtype, int M, int N, int K, const void *A, const 
         int r = M, k = K;
         int *out = sums;
         void *args[] = {&x, &r, &k, &out};
-        e = hipLaunchKernel(fn, dim3(M), dim3(256), args, 0, stream);
+        const hipError_t e = hipLaunchKernel(fn, dim3(M), dim3(256), args, 0, stream);
         if (e != hipSuccess) return e;
         epi.sum_a = out;
     }
@@ -496,7 +435,7 @@ hipError_t zero_point_sums(int dtype, int M, int N, int K, const void *A, const 
         int r = N, k = K;
         int *out = sums + M;
         void *args[] = {&x, &r, &k, &out};
-        e = hipLaunchKernel(fn, dim3(N), dim3(256), args, 0, stream);
+        const hipError_t e = hipLaunchKernel(fn, dim3(N), dim3(256), args, 0, stream);
         if (e != hipSuccess) return e;
         epi.sum_b = out;
     }
@@ -518,22 +457,54 @@ bool valid_epilogue(int dtype, const mpgemm_epilogue *e) {
     return true;
 }
 
+// The kernel choice of a call: variant (< 0: the automatic selection) and
+// splits (< 0: the automatic choice, which splits only when the workspace
+// holds the split's scratch), validated; the workspace plan of that choice.
+struct Choice {
+    int variant, splits;
+    WsPlan plan;
+};
+
+hipError_t choose(int dtype, int variant, int splits, int M, int N, int K, const void *A, const void *B,
+                  const void *C, bool zero_points, size_t ws_bytes, Choice &out) {
+    const Variant *t = table(dtype);
+    if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
+    if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
+    if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
+    if (splits < 0) {
+        splits = choose_splits(dtype, t[variant], M, N, K);
+        if (splits > 1 && ws_plan(t[variant], splits, M, N, K, zero_points).total > ws_bytes) splits = 1;
+    }
+    if (!splits_ok(dtype, t[variant], M, N, K, splits)) return hipErrorInvalidValue;
+    out = Choice{variant, splits, ws_plan(t[variant], splits, M, N, K, zero_points)};
+    return hipSuccess;
+}
+
 // variant < 0: the selection; splits < 0: the automatic choice for the variant.
-hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const void *A,
-               const void *B, void *C, hipStream_t stream, const mpgemm_epilogue *scaled = nullptr) {
+hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const void *A, const void *B, void *C,
+               hipStream_t stream, const mpgemm_epilogue *scaled, Ws ws) {
     int c_elem = 4;
     if (scaled) {
         if (dtype < F16 || dtype > S4 || !valid_epilogue(dtype, scaled)) return hipErrorInvalidValue;
         c_elem = scaled->out_type == MPGEMM_OUT_F32 ? 4 : 2;
     }
     if (!valid_args(dtype, M, N, K, A, B, C, c_elem)) return hipErrorInvalidValue;
+    if (!ws.p) ws.bytes = 0;
+    if (ws.bytes && !aligned(ws.p, kWsAlign)) return hipErrorInvalidValue;
     if (M == 0 || N == 0) return hipSuccess;
-    const Variant *t = table(dtype);
-    if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
-    if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
-    if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
-    if (splits < 0) splits = choose_splits(dtype, t[variant], M, N, K);
-    if (!splits_ok(dtype, t[variant], M, N, K, splits)) return hipErrorInvalidValue;
+    if (ws.bytes) {
+        // the workspace must not overlap the operands or the output
+        const uint64_t rb = (uint64_t)row_bytes(dtype, K);
+        if (uintptr_t(-1) - reinterpret_cast<uintptr_t>(ws.p) < ws.bytes) return hipErrorInvalidValue;
+        if (overlap(ws.p, ws.bytes, C, (uint64_t)M * (uint64_t)N * (uint64_t)c_elem) ||
+            (K > 0 && (overlap(ws.p, ws.bytes, A, (uint64_t)M * rb) || overlap(ws.p, ws.bytes, B, (uint64_t)N * rb))))
+            return hipErrorInvalidValue;
+    }
+    const bool zp = scaled && (scaled->zero_a || scaled->zero_b);
+    Choice ch;
+    hipError_t e = choose(dtype, variant, splits, M, N, K, A, B, C, zp, ws.bytes, ch);
+    if (e != hipSuccess) return e;
+    if (ch.plan.total > ws.bytes) return hipErrorInvalidValue;  // scratch needed, no (large enough) workspace
     EpiParams epi = plain_epilogue(K);
     if (scaled) {
         epi.scale_a = scaled->scale_a;
@@ -541,10 +512,10 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
         epi.zero_a = scaled->zero_a;
         epi.zero_b = scaled->zero_b;
         epi.out = scaled->out_type;
-        const hipError_t e = zero_point_sums(dtype, M, N, K, A, B, epi, stream);
+        e = zero_point_sums(dtype, M, N, K, A, B, epi, reinterpret_cast<int *>(ws.p + ch.plan.sums_off), stream);
         if (e != hipSuccess) return e;
     }
-    return launch(dtype, t[variant], splits, M, N, K, A, B, C, epi, stream);
+    return launch(dtype, table(dtype)[ch.variant], ch.splits, M, N, K, A, B, C, epi, ch.plan, ws, stream);
 }
 
 }  // namespace
@@ -558,7 +529,7 @@ hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const v
     // occupies K * N elements either way)
     if (!valid_args(dtype, M, N, K, A, B, C)) return hipErrorInvalidValue;
     if (M == 0 || N == 0) return hipSuccess;
-    if (K == 0) return run(dtype, -1, -1, M, N, K, A, B, C, stream);  // zero fill
+    if (K == 0) return run(dtype, -1, -1, M, N, K, A, B, C, stream, nullptr, Ws{nullptr, 0});  // zero fill
     typedef TileCfg<256, 256, 2, 4, 128, 2, 4> T;
     const long kb = row_bytes(dtype, K);
     if (N % T::BN || kb % T::BKB || !aligned(A, 16) || !aligned(B, 16)) return hipErrorInvalidValue;
@@ -573,17 +544,53 @@ hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const v
 
 hipError_t gemm_f16_f32(int M, int N, int K, const void *A, const void *B, float *C,
                         hipStream_t stream) {
-    return run(F16, -1, -1, M, N, K, A, B, C, stream);
+    return run(F16, -1, -1, M, N, K, A, B, C, stream, nullptr, Ws{nullptr, 0});
 }
 
 hipError_t gemm_s8_s32(int M, int N, int K, const int8_t *A, const int8_t *B, int32_t *C,
                        hipStream_t stream) {
-    return run(S8, -1, -1, M, N, K, A, B, C, stream);
+    return run(S8, -1, -1, M, N, K, A, B, C, stream, nullptr, Ws{nullptr, 0});
 }
 
 hipError_t gemm_s4_s32(int M, int N, int K, const uint8_t *A, const uint8_t *B, int32_t *C,
                        hipStream_t stream) {
-    return run(S4, -1, -1, M, N, K, A, B, C, stream);
+    return run(S4, -1, -1, M, N, K, A, B, C, stream, nullptr, Ws{nullptr, 0});
+}
+
+hipError_t gemm_scaled(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                       const mpgemm_epilogue *epi, hipStream_t stream) {
+    if (!epi) return hipErrorInvalidValue;
+    return run(dtype, -1, -1, M, N, K, A, B, C, stream, epi, Ws{nullptr, 0});
+}
+
+hipError_t mpgemm_gemm_ws(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                          const mpgemm_epilogue *epi, void *workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+    return run(dtype, -1, -1, M, N, K, A, B, C, stream, epi,
+               Ws{static_cast<uint8_t *>(workspace), workspace_bytes});
+}
+
+hipError_t mpgemm_workspace_size(int dtype, int variant, int splits, int M, int N, int K,
+                                 const mpgemm_epilogue *epi, size_t *bytes) {
+    if (!bytes || splits < 0) return hipErrorInvalidValue;
+    int c_elem = 4;
+    if (epi) {
+        if (dtype < F16 || dtype > S4 || !valid_epilogue(dtype, epi)) return hipErrorInvalidValue;
+        c_elem = epi->out_type == MPGEMM_OUT_F32 ? 4 : 2;
+    }
+    // sizes only: stand-in pointers, 256-byte aligned and far apart
+    const void *A = reinterpret_cast<const void *>(uintptr_t(1) << 20);
+    const void *B = reinterpret_cast<const void *>(uintptr_t(1) << 44);
+    const void *C = reinterpret_cast<const void *>(uintptr_t(1) << 46);
+    if (!valid_args(dtype, M, N, K, A, B, C, c_elem)) return hipErrorInvalidValue;
+    *bytes = 0;
+    if (M == 0 || N == 0) return hipSuccess;
+    Choice ch;
+    const bool zp = epi && (epi->zero_a || epi->zero_b);
+    const hipError_t e = choose(dtype, variant, splits == 0 ? -1 : splits, M, N, K, A, B, C, zp, SIZE_MAX, ch);
+    if (e != hipSuccess) return e;
+    *bytes = ch.plan.total;
+    return hipSuccess;
 }
 
 int mpgemm_num_variants(int dtype) { return num_variants(dtype); }
@@ -612,7 +619,15 @@ int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const v
 hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const void *A,
                               const void *B, void *C, hipStream_t stream) {
     if (variant < 0) return hipErrorInvalidValue;
-    return run(dtype, variant, -1, M, N, K, A, B, C, stream);
+    return run(dtype, variant, -1, M, N, K, A, B, C, stream, nullptr, Ws{nullptr, 0});
+}
+
+hipError_t mpgemm_run_variant_ws(int dtype, int variant, int splits, int M, int N, int K, const void *A,
+                                 const void *B, void *C, const mpgemm_epilogue *epi, void *workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+    if (variant < 0 || splits < 0) return hipErrorInvalidValue;
+    return run(dtype, variant, splits == 0 ? -1 : splits, M, N, K, A, B, C, stream, epi,
+               Ws{static_cast<uint8_t *>(workspace), workspace_bytes});
 }
 
 int mpgemm_select_splits(int dtype, int variant, int M, int N, int K) {
@@ -624,12 +639,6 @@ int mpgemm_select_splits(int dtype, int variant, int M, int N, int K) {
     return choose_splits(dtype, t[variant], M, N, K);
 }
 
-hipError_t mpgemm_run_variant_splits(int dtype, int variant, int splits, int M, int N, int K,
-                                     const void *A, const void *B, void *C, hipStream_t stream) {
-    if (variant < 0 || splits < 1) return hipErrorInvalidValue;
-    return run(dtype, variant, splits, M, N, K, A, B, C, stream);
-}
-
 void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out) {
     uint32_t w[4] = {0, 0, 0, 0}, o[6];
     for (int e = 0; e < 16; ++e) w[e >> 2] |= (uint32_t)in[e] << (8 * (e & 3));
@@ -637,17 +646,11 @@ void mpgemm_s4_run_to_fp6(const uint8_t *in, uint32_t *out) {
     for (int i = 0; i < 6; ++i) out[i] = o[i];
 }
 
-hipError_t gemm_scaled(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
-                       const mpgemm_epilogue *epi, hipStream_t stream) {
-    if (!epi) return hipErrorInvalidValue;
-    return run(dtype, -1, -1, M, N, K, A, B, C, stream, epi);
-}
-
-hipError_t mpgemm_run_variant_scaled(int dtype, int variant, int splits, int M, int N, int K,
-                                     const void *A, const void *B, void *C,
-                                     const mpgemm_epilogue *epi, hipStream_t stream) {
-    if (variant < 0 || splits < 0 || !epi) return hipErrorInvalidValue;
-    return run(dtype, variant, splits == 0 ? -1 : splits, M, N, K, A, B, C, stream, epi);
+void mpgemm_s4_run_to_e2m3(const uint8_t *in, uint32_t *out) {
+    uint32_t w[4] = {0, 0, 0, 0}, o[6];
+    for (int e = 0; e < 16; ++e) w[e >> 2] |= (uint32_t)in[e] << (8 * (e & 3));
+    s4_run_to_e2m3(w, o);
+    for (int i = 0; i < 6; ++i) out[i] = o[i];
 }
 
 }  // extern "C"

@@ -14,6 +14,7 @@
 #include "skinny_gemm.hpp"
 #include "wide_gemm.hpp"
 #include "wide_f6.hpp"
+#include "wide_i4.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -61,7 +62,7 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5, I4WIDE = 6 };
 
 struct Variant {
     const char *name;
@@ -72,6 +73,9 @@ struct Variant {
     int threads;
     const void *fn;
     bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
+    const void *fn_epi = nullptr;  // WIDE, FP6WIDE, I4WIDE: the instantiation with the
+                                   // shared epilogue (ragged edges, scaled outputs); fn
+                                   // stores raw sums of whole tiles
 };
 
 typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int,
@@ -126,15 +130,27 @@ Variant skinny(const char *name) {
 }
 
 // One wave per SIMD, 256 x 256 tiles only (wide_gemm.hpp); FP16 and INT8 (no
-// kernel for INT4: fn is null and the variant supports nothing).
-template <int DT>
+// kernel for INT4: fn is null and the variant supports nothing). AUX: cache
+// policy of the copy loads.
+template <int DT, int AUX = CP_DEFAULT>
 Variant wide(const char *name) {
-    const void *f = nullptr;
+    const void *f = nullptr, *fe = nullptr;
     if constexpr (DT == F16 || DT == S8) {
-        kernel_fn k = &wide_gemm<DT>;
+        kernel_fn k = &wide_gemm<DT, true, AUX>, ke = &wide_gemm<DT, false, AUX>;
         f = reinterpret_cast<const void *>(k);
+        fe = reinterpret_cast<const void *>(ke);
     }
-    return Variant{name, WIDE, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false};
+    return Variant{name, WIDE, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false, fe};
+}
+
+// INT4 on the FP6 cores with the conversion inside the GEMM (wide_i4.hpp);
+// bkb holds the K multiple it needs (in elements). AUX: cache policy of the
+// operand loads.
+template <int AUX = CP_DEFAULT>
+Variant i4wide(const char *name) {
+    kernel_fn k = &wide_i4_gemm<true, AUX>, ke = &wide_i4_gemm<false, AUX>;
+    return Variant{name, I4WIDE, WideI4Cfg::BM, WideI4Cfg::BN, 256, WideI4Cfg::NTHREADS,
+                   reinterpret_cast<const void *>(k), false, reinterpret_cast<const void *>(ke)};
 }
 
 template <class T>
@@ -151,9 +167,9 @@ Variant fp6(const char *name) {
 inline Variant fp6wide(const char *name) {
     typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
                           int32_t *, int, int, int, int, int, int, int, EpiParams);
-    f6_fn f = &wide_f6_gemm<true>;
+    f6_fn f = &wide_f6_gemm<true>, fe = &wide_f6_gemm<false>;
     return Variant{name, FP6WIDE, WideF6Cfg::BM, WideF6Cfg::BN, WideF6Cfg::J, WideF6Cfg::NTHREADS,
-                   reinterpret_cast<const void *>(f), false};
+                   reinterpret_cast<const void *>(f), false, reinterpret_cast<const void *>(fe)};
 }
 
 template <int DT>
@@ -213,12 +229,15 @@ Variant generic(const char *name) {
      pipelined<DT, T64x32_w2_m16, true>("spread64x32_w2x1_k128_s4_m16"),  \
      pipelined<DT, T128x32_w4_m16, true>("spread128x32_w4x1_k128_s4_m16"), \
      pipelined<DT, T128x64_w4, true>("spread128x64_w2x2_k128_s4"),        \
-     wide<DT>("wide256x256_w2x2_k128_m16")
+     wide<DT>("wide256x256_w2x2_k128_m16"),                                \
+     wide<DT, CP_SC0>("wide256x256_w2x2_k128_m16_sc0"),                    \
+     wide<DT, CP_SC1>("wide256x256_w2x2_k128_m16_sc1"),                    \
+     wide<DT, CP_NT>("wide256x256_w2x2_k128_m16_nt")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 51;
-constexpr int kNumFp6 = 9;
+constexpr int kNumCommon = 54;
+constexpr int kNumFp6 = 13;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 
 // Kernel of the transposed-B entry point (tposeb.hip): F16 or S8, else null.

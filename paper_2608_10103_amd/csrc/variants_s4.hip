@@ -3,7 +3,9 @@
 
 namespace mpg {
 
-// INT4 also runs on the FP6 matrix cores (f6_gemm.hpp); "k" is k per stage.
+// INT4 also runs on the FP6 matrix cores: converted by a pre-pass into a
+// workspace (f6_gemm.hpp, wide_f6.hpp; "k" is k per stage) or inside the GEMM
+// (wide_i4.hpp).
 const Variant kS4[] = {VARIANT_LIST(S4),
                              fp6<F6_256x256_w8_s3>("fp6pipe256x256_w2x4_k128_s3"),
                              fp6<F6_256x256_w8_s2>("fp6pipe256x256_w2x4_k128_s2"),
@@ -13,7 +15,12 @@ const Variant kS4[] = {VARIANT_LIST(S4),
                              fp6<F6_128x128_w4_s4>("fp6pipe128x128_w2x2_k128_s4"),
                              fp6<F6_128x128_w4_s6>("fp6pipe128x128_w2x2_k128_s6"),
                              fp6<F6_128x128_w4_k256_s3>("fp6pipe128x128_w2x2_k256_s3"),
-                             fp6wide("fp6wide256x256_w2x2_k128_s3")};
+                             fp6wide("fp6wide256x256_w2x2_k128_s3"),
+                             // conversion inside the GEMM (no workspace); "k": K multiple
+                             i4wide("e2m3wide256x256_w2x2_k256"),
+                             i4wide<CP_SC0>("e2m3wide256x256_w2x2_k256_sc0"),
+                             i4wide<CP_SC1>("e2m3wide256x256_w2x2_k256_sc1"),
+                             i4wide<CP_NT>("e2m3wide256x256_w2x2_k256_nt")};
 static_assert(sizeof(kS4) / sizeof(kS4[0]) == kNumS4, "variant count out of date in variants.hpp");
 
 }  // namespace mpg

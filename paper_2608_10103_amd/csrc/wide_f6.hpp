@@ -151,7 +151,8 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
     // zeroed accumulators into their AGPRs in order, then wait states before
-    // the first assembly MFMA reads them (the compiler does not insert them)
+    // the first assembly MFMA reads them (the compiler does not insert them;
+    // a VALU write of an MFMA's accumulator input needs 2, the nop gives 5)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -186,9 +187,17 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
         wf6_chunk<0>(ra[1], rb[1], acc, ra[0], rb[0], lds, pa0 + nxt, qa0 + nxt, pb0 + nxt, qb0 + nxt, c,
                      min(kt + 3, KT - 1), s0);
     }
-    // clamped copies may still be landing; the last MFMA results (the
-    // compiler does not track the assembly MFMAs: 16 passes at most)
+    // Clamped copies may still be landing. The last MFMA results: an XDL op
+    // of P passes (P = 8 for the 32x32x64 FP6 MFMA, 16 for FP8) needs P + 3
+    // wait states before a VALU or memory instruction reads its destination,
+    // and the compiler does not count them for the assembly MFMAs; the nops
+    // give 40. The empty asm statements then order every read of the
+    // accumulators after the nops.
     asm volatile("s_waitcnt vmcnt(0)\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc[i][j]));
 
     const long row0 = (long)tm * T::BM + wm * 128;
     const long col0 = (long)tn * T::BN + wn * 128 + r;

@@ -53,14 +53,20 @@ struct WideCfg {
     static_assert(LDS_BYTES <= 160 * 1024, "LDS capacity");
 };
 
+// Cache policy of the copy loads (the instruction's cache-policy bits: sc0 =
+// 1, nt = 2, sc1 = 16; 0 = the default policy), the CDNA4 counterpart of the
+// paper's cp.async .ca / .cg choice (Run 4).
+enum CachePolicy : int { CP_DEFAULT = 0, CP_SC0 = 1, CP_NT = 2, CP_SC1 = 16 };
+
 // One wave-wide direct-to-LDS buffer load: lane l copies 16 bytes from
 // base + voff + soff (voff its own, soff wave-uniform) to lds + 16 l; `bytes`
 // bounds the buffer (loads past it read zeros). Device pass only.
+template <int AUX = CP_DEFAULT>
 __device__ __forceinline__ void wide_copy(const uint8_t *base, int bytes, uint8_t *lds, uint32_t voff, int soff) {
 #if defined(__HIP_DEVICE_COMPILE__)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, bytes, 0x00020000), (lds_void *)lds, 16,
-        (int)voff, soff, 0, 0);
+        (int)voff, soff, 0, AUX);
 #endif
 }
 
@@ -84,14 +90,15 @@ struct WideCopy {
 };
 
 // copy load j (0..15) of slice ks into buffer b
+template <int AUX>
 __device__ __forceinline__ void wide_load(const WideCopy &c, int j, int ks, int b) {
-    wide_copy(c.panel, c.bytes, c.dst + b * WideCfg::STAGE + j * WideCfg::BLK, c.voff, ks * WideCfg::BKB + j * c.kb);
+    wide_copy<AUX>(c.panel, c.bytes, c.dst + b * WideCfg::STAGE + j * WideCfg::BLK, c.voff, ks * WideCfg::BKB + j * c.kb);
 }
 
 // Groups [G0, G1) of one K-chunk CH: MFMAs on (a, b); reads of the 16 runs
 // of the next operands into (na, nb) in groups [R0, R0 + 6); copy loads as in
 // the schedule above (slice k1 = kt + 1, k2 = kt + 2, clamped).
-template <int DT, int CH, int R0, int G0, int G1>
+template <int DT, int CH, int R0, int G0, int G1, int AUX>
 __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b)[8],
                                             typename Acc<DT, 16>::type (&acc)[8][8], i32x4 (&na)[8],
                                             i32x4 (&nb)[8], const uint8_t *rab, const uint8_t *rbb,
@@ -109,10 +116,10 @@ __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b
             });
         }
         if constexpr (g % 2 == 0) {
-            if constexpr (CH == 0 && g < 8) wide_load(c, 12 + g / 2, k1, (kt + 1) & 1);
-            if constexpr (CH == 0 && g >= 8) wide_load(c, (g - 8) / 2, k2, kt & 1);
-            if constexpr (CH == 1 && g < 8) wide_load(c, 4 + g / 2, k2, kt & 1);
-            if constexpr (CH == 1 && g >= 8) wide_load(c, 8 + (g - 8) / 2, k2, kt & 1);
+            if constexpr (CH == 0 && g < 8) wide_load<AUX>(c, 12 + g / 2, k1, (kt + 1) & 1);
+            if constexpr (CH == 0 && g >= 8) wide_load<AUX>(c, (g - 8) / 2, k2, kt & 1);
+            if constexpr (CH == 1 && g < 8) wide_load<AUX>(c, 4 + g / 2, k2, kt & 1);
+            if constexpr (CH == 1 && g >= 8) wide_load<AUX>(c, 8 + (g - 8) / 2, k2, kt & 1);
         }
         __builtin_amdgcn_sched_barrier(0);
     });
@@ -120,8 +127,9 @@ __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b
 
 // PLAIN: raw sums to the row-major output (the entry points' common case),
 // stored straight from the accumulators; otherwise the shared epilogue with
-// scales, zero points and output types (see EpiParams).
-template <int DT, bool PLAIN = true>
+// scales, zero points and output types (see EpiParams). AUX: cache policy
+// of the copy loads.
+template <int DT, bool PLAIN = true, int AUX = CP_DEFAULT>
 __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t *__restrict__ A,
                                                                  const uint8_t *__restrict__ B,
                                                                  void *__restrict__ Cv, int M, int N, int Kb,
@@ -159,7 +167,8 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     // The zeroed accumulators are written to the AGPRs here (each empty asm
     // takes its block in AGPRs, in order), then wait states before the first
     // assembly MFMA reads them: the compiler does not insert them for
-    // assembly it does not know is an MFMA.
+    // assembly it does not know is an MFMA. A VALU write of a register an
+    // MFMA then reads as its accumulator needs 2 wait states; the nop gives 5.
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -169,9 +178,9 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     const int KT = Kb / T::BKB;
     // prologue: slice 0 whole, loads 0-11 of slice 1; wait for slice 0
 #pragma unroll
-    for (int j = 0; j < 16; ++j) wide_load(c, j, 0, 0);
+    for (int j = 0; j < 16; ++j) wide_load<AUX>(c, j, 0, 0);
 #pragma unroll
-    for (int j = 0; j < 12; ++j) wide_load(c, j, min(1, KT - 1), 1);
+    for (int j = 0; j < 12; ++j) wide_load<AUX>(c, j, min(1, KT - 1), 1);
     asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
     i32x4 ra[2][8], rb[2][8];
 #pragma unroll
@@ -184,16 +193,24 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
         const int k1 = min(kt + 1, KT - 1), k2 = min(kt + 2, KT - 1);
         const uint8_t *r1a = ra0 + cur + 64, *r1b = rb0 + cur + 64;  // chunk 1 of slice kt
         const uint8_t *r0a = ra0 + nxt, *r0b = rb0 + nxt;            // chunk 0 of slice kt + 1
-        wide_groups<DT, 0, 0, 0, 8>(ra[0], rb[0], acc, ra[1], rb[1], r1a, r1b, c, k1, k2, kt);
+        wide_groups<DT, 0, 0, 0, 8, AUX>(ra[0], rb[0], acc, ra[1], rb[1], r1a, r1b, c, k1, k2, kt);
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        wide_groups<DT, 0, 0, 8, 16>(ra[0], rb[0], acc, ra[1], rb[1], r1a, r1b, c, k1, k2, kt);
-        wide_groups<DT, 1, 8, 0, 8>(ra[1], rb[1], acc, ra[0], rb[0], r0a, r0b, c, k1, k2, kt);
+        wide_groups<DT, 0, 0, 8, 16, AUX>(ra[0], rb[0], acc, ra[1], rb[1], r1a, r1b, c, k1, k2, kt);
+        wide_groups<DT, 1, 8, 0, 8, AUX>(ra[1], rb[1], acc, ra[0], rb[0], r0a, r0b, c, k1, k2, kt);
         asm volatile("s_waitcnt vmcnt(8)\n\ts_barrier" ::: "memory");
-        wide_groups<DT, 1, 8, 8, 16>(ra[1], rb[1], acc, ra[0], rb[0], r0a, r0b, c, k1, k2, kt);
+        wide_groups<DT, 1, 8, 8, 16, AUX>(ra[1], rb[1], acc, ra[0], rb[0], r0a, r0b, c, k1, k2, kt);
     }
-    // clamped copies may still be landing; the last MFMA results (the compiler
-    // does not track the assembly MFMAs: 8 passes of 4 cycles at most)
+    // Clamped copies may still be landing. The last MFMA results: an XDL op
+    // of P passes (P = 8 for the 16x16 FP16 and INT8 MFMAs here) needs
+    // P + 3 wait states before a VALU or memory instruction reads its
+    // destination, and the compiler does not count them for the assembly
+    // MFMAs; the nops give 32. The empty asm statements then order every
+    // read of the accumulators after the nops.
     asm volatile("s_waitcnt vmcnt(0)\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
 
     const long row0 = (long)tm * T::BM + wm * 128;
     const long col0 = (long)tn * T::BN + wn * 128 + r;

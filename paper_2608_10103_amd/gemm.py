@@ -6,6 +6,12 @@ given stream. PyTorch supplies device memory and streams; no torch operator
 runs on the GPU path. If the library is not built this module raises instead
 of computing anything another way.
 
+Scratch memory: the plain entry points use none. Calls that need some (an
+explicit split K, the INT4 variants fed by an FP6 pre-pass, zero points) take
+a workspace: a zero-filled uint8 CUDA tensor (new_workspace), or
+workspace="auto" to have this module allocate one through PyTorch for the
+call. The library itself never allocates.
+
 Operand conventions (see include/mpgemm.h):
   A  (M, K)    row-major          float16 / int8, or uint8 (M, K/2) for INT4
   B  (N, K)    = K x N column-major, same dtypes (uint8 (N, K/2) for INT4)
@@ -59,23 +65,30 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_run_variant.restype = I
     L.mpgemm_select_splits.argtypes = [I, I, I, I, I]
     L.mpgemm_select_splits.restype = I
-    L.mpgemm_run_variant_splits.argtypes = [I, I, I, I, I, I, P, P, P, P]
-    L.mpgemm_run_variant_splits.restype = I
     L.gemm_scaled.argtypes = [I, I, I, I, P, P, P, P, P]
     L.gemm_scaled.restype = I
-    L.mpgemm_run_variant_scaled.argtypes = [I, I, I, I, I, I, P, P, P, P, P]
-    L.mpgemm_run_variant_scaled.restype = I
+    S = ctypes.c_size_t
+    L.mpgemm_gemm_ws.argtypes = [I, I, I, I, P, P, P, P, P, S, P]
+    L.mpgemm_gemm_ws.restype = I
+    L.mpgemm_run_variant_ws.argtypes = [I, I, I, I, I, I, P, P, P, P, P, S, P]
+    L.mpgemm_run_variant_ws.restype = I
+    L.mpgemm_workspace_size.argtypes = [I, I, I, I, I, I, P, ctypes.POINTER(S)]
+    L.mpgemm_workspace_size.restype = I
     L.mpgemm_s4_run_to_fp6.argtypes = [P, P]
-    L.mpgemm_gemm_bt.argtypes = [I, I, I, I, P, P, P, P]
     L.mpgemm_s4_run_to_fp6.restype = None
+    L.mpgemm_s4_run_to_e2m3.argtypes = [P, P]
+    L.mpgemm_s4_run_to_e2m3.restype = None
+    L.mpgemm_gemm_bt.argtypes = [I, I, I, I, P, P, P, P]
+    L.mpgemm_gemm_bt.restype = I
     _lib = L
     return L
 
 
-EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "mpgemm_num_variants",
-                    "mpgemm_variant_name", "mpgemm_select_variant", "mpgemm_variant_supports",
-                    "mpgemm_run_variant", "mpgemm_select_splits", "mpgemm_run_variant_splits",
-                    "gemm_scaled", "mpgemm_run_variant_scaled", "mpgemm_s4_run_to_fp6", "mpgemm_gemm_bt")
+EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "gemm_scaled", "mpgemm_gemm_ws",
+                    "mpgemm_workspace_size", "mpgemm_num_variants", "mpgemm_variant_name",
+                    "mpgemm_select_variant", "mpgemm_variant_supports", "mpgemm_run_variant",
+                    "mpgemm_select_splits", "mpgemm_run_variant_ws", "mpgemm_s4_run_to_fp6",
+                    "mpgemm_s4_run_to_e2m3", "mpgemm_gemm_bt")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -113,42 +126,87 @@ def _out(dtype, M, N, A, C):
     return C
 
 
-def _call(dtype: str, A, B, C, stream, variant, splits=None):
+def workspace_size(dtype: str, M: int, N: int, K: int, variant=None, splits=None, epi=None) -> int:
+    """Bytes of workspace a call would use (mpgemm_workspace_size): the
+    automatic choice (variant None, splits None) or an explicit one; epi an
+    Epilogue or None. Raises HipError for arguments the call would refuse."""
+    out = ctypes.c_size_t(0)
+    code = lib().mpgemm_workspace_size(DTYPE_CODE[dtype], -1 if variant is None else variant, splits or 0,
+                                       M, N, K, None if epi is None else ctypes.addressof(epi),
+                                       ctypes.byref(out))
+    if code != 0:
+        raise HipError(code, f"workspace size of {dtype} {M}x{N}x{K}")
+    return int(out.value)
+
+
+def new_workspace(nbytes: int, device) -> torch.Tensor:
+    """A zero-filled workspace (uint8 CUDA tensor) of at least nbytes; PyTorch's
+    allocations are 256-byte aligned, as the library requires."""
+    return torch.zeros(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def _workspace(workspace, dtype, M, N, K, variant, splits, epi, device, stream):
+    """(pointer, bytes, tensor) of a workspace argument: None, "auto" (allocated
+    here through PyTorch, zero-filled, its memory kept from reuse until the
+    call's stream has done with it) or a uint8 CUDA tensor."""
+    if workspace is None:
+        return None, 0, None
+    if isinstance(workspace, str):
+        if workspace != "auto":
+            raise ValueError('workspace must be None, "auto" or a uint8 CUDA tensor')
+        n = workspace_size(dtype, M, N, K, variant, splits, epi)
+        if n == 0:
+            return None, 0, None
+        workspace = new_workspace(n, device)
+        if stream is not None:
+            workspace.record_stream(stream)
+    if (not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8 or not workspace.is_cuda
+            or not workspace.is_contiguous() or workspace.device != device):
+        raise ValueError(f"workspace must be a contiguous uint8 tensor on {device}")
+    return workspace.data_ptr(), workspace.numel(), workspace
+
+
+def _call(dtype: str, A, B, C, stream, variant, splits=None, workspace=None):
     M, N, K = _shapes(dtype, A, B)
     C = _out(dtype, M, N, A, C)
     s = _stream_ptr(stream, A.device)
+    if splits is not None and variant is None:
+        raise ValueError("splits needs an explicit variant")
+    wp, wn, _keep = _workspace(workspace, dtype, M, N, K, variant, splits, None, A.device, stream)
     with torch.cuda.device(A.device):
-        if variant is None:
-            if splits is not None:
-                raise ValueError("splits needs an explicit variant")
-            fn = getattr(lib(), {"f16": "gemm_f16_f32", "s8": "gemm_s8_s32",
-                                 "s4": "gemm_s4_s32"}[dtype])
-            code = fn(M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
-        elif splits is None:
-            code = lib().mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, A.data_ptr(),
-                                            B.data_ptr(), C.data_ptr(), s)
+        if wn == 0 and splits is None:
+            if variant is None:
+                fn = getattr(lib(), {"f16": "gemm_f16_f32", "s8": "gemm_s8_s32",
+                                     "s4": "gemm_s4_s32"}[dtype])
+                code = fn(M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
+            else:
+                code = lib().mpgemm_run_variant(DTYPE_CODE[dtype], variant, M, N, K, A.data_ptr(),
+                                                B.data_ptr(), C.data_ptr(), s)
+        elif variant is None:
+            code = lib().mpgemm_gemm_ws(DTYPE_CODE[dtype], M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                        None, wp, wn, s)
         else:
-            code = lib().mpgemm_run_variant_splits(DTYPE_CODE[dtype], variant, splits, M, N, K,
-                                                   A.data_ptr(), B.data_ptr(), C.data_ptr(), s)
+            code = lib().mpgemm_run_variant_ws(DTYPE_CODE[dtype], variant, splits or 0, M, N, K, A.data_ptr(),
+                                               B.data_ptr(), C.data_ptr(), None, wp, wn, s)
     if code != 0:
         raise HipError(code, f"{dtype} GEMM {M}x{N}x{K}")
     return C
 
 
-def gemm_f16_f32(A, B, C=None, stream=None, variant=None, splits=None):
+def gemm_f16_f32(A, B, C=None, stream=None, variant=None, splits=None, workspace=None):
     """C = A @ B with FP16 A (M, K), FP16 B (N, K) = K x N column-major; FP32 C."""
-    return _call("f16", A, B, C, stream, variant, splits)
+    return _call("f16", A, B, C, stream, variant, splits, workspace)
 
 
-def gemm_s8_s32(A, B, C=None, stream=None, variant=None, splits=None):
+def gemm_s8_s32(A, B, C=None, stream=None, variant=None, splits=None, workspace=None):
     """C = A @ B with INT8 A (M, K), INT8 B (N, K); INT32 C."""
-    return _call("s8", A, B, C, stream, variant, splits)
+    return _call("s8", A, B, C, stream, variant, splits, workspace)
 
 
-def gemm_s4_s32(A, B, C=None, stream=None, variant=None, splits=None):
+def gemm_s4_s32(A, B, C=None, stream=None, variant=None, splits=None, workspace=None):
     """C = A @ B with packed INT4 A (M, K/2) and B (N, K/2) uint8 (low nibble =
     even k); INT32 C."""
-    return _call("s4", A, B, C, stream, variant, splits)
+    return _call("s4", A, B, C, stream, variant, splits, workspace)
 
 
 GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
@@ -199,11 +257,12 @@ def _vec(x, n, dtype, name, device):
 
 
 def gemm_scaled(dtype: str, A, B, scale_a=None, scale_b=None, zero_a=None, zero_b=None,
-                out_dtype=torch.float16, C=None, stream=None, variant=None, splits=None):
+                out_dtype=torch.float16, C=None, stream=None, variant=None, splits=None, workspace=None):
     """C = round(scale_a[i] * scale_b[j] * sum_k (A(i,k) - zero_a[i]) (B(k,j) - zero_b[j]))
     in out_dtype (float32, float16 or bfloat16); operands as for GEMM[dtype];
     scales float32 (M,) / (N,), zero points int32 (M,) / (N,) (integer inputs
-    only), any of them None. Runs in the GEMM kernels' epilogue."""
+    only; they need a workspace), any of them None. Runs in the GEMM kernels'
+    epilogue."""
     M, N, K = _shapes(dtype, A, B)
     if out_dtype not in OUT_TYPE:
         raise ValueError("out_dtype must be float32, float16 or bfloat16")
@@ -215,17 +274,21 @@ def gemm_scaled(dtype: str, A, B, scale_a=None, scale_b=None, zero_a=None, zero_
         C = torch.empty((M, N), dtype=out_dtype, device=dev)
     elif C.dtype != out_dtype or tuple(C.shape) != (M, N) or not C.is_contiguous() or C.device != dev:
         raise ValueError(f"C must be a contiguous ({M}, {N}) {out_dtype} tensor on {dev}")
+    if splits is not None and variant is None:
+        raise ValueError("splits needs an explicit variant")
+    wp, wn, _keep = _workspace(workspace, dtype, M, N, K, variant, splits, epi, dev, stream)
     s = _stream_ptr(stream, dev)
     with torch.cuda.device(dev):
-        if variant is None:
-            if splits is not None:
-                raise ValueError("splits needs an explicit variant")
+        if variant is None and wn == 0:
             code = lib().gemm_scaled(DTYPE_CODE[dtype], M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(),
                                      ctypes.addressof(epi), s)
+        elif variant is None:
+            code = lib().mpgemm_gemm_ws(DTYPE_CODE[dtype], M, N, K, A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                        ctypes.addressof(epi), wp, wn, s)
         else:
-            code = lib().mpgemm_run_variant_scaled(DTYPE_CODE[dtype], variant, splits or 0, M, N, K,
-                                                   A.data_ptr(), B.data_ptr(), C.data_ptr(),
-                                                   ctypes.addressof(epi), s)
+            code = lib().mpgemm_run_variant_ws(DTYPE_CODE[dtype], variant, splits or 0, M, N, K,
+                                               A.data_ptr(), B.data_ptr(), C.data_ptr(),
+                                               ctypes.addressof(epi), wp, wn, s)
     if code != 0:
         raise HipError(code, f"scaled {dtype} GEMM {M}x{N}x{K}")
     return C
@@ -272,6 +335,18 @@ def variant_supports(dtype: str, variant: int, M: int, N: int, K: int, a_ptr: in
                      b_ptr: int = 1 << 40, c_ptr: int = 1 << 44) -> bool:
     return lib().mpgemm_variant_supports(DTYPE_CODE[dtype], variant, M, N, K, a_ptr, b_ptr,
                                          c_ptr) == 1
+
+
+def s4_run_to_e2m3(run: bytes) -> list:
+    """Host-side INT4 -> biased FP6 E2M3 conversion of one 16-byte run (the
+    conversion the INT4 kernel applies inside the GEMM): the six 32-bit words
+    of the 192-bit string of 32 six-bit codes (code = nibble ^ 8)."""
+    if len(run) != 16:
+        raise ValueError("a run is 16 bytes")
+    src = (ctypes.c_uint8 * 16)(*run)
+    out = (ctypes.c_uint32 * 6)()
+    lib().mpgemm_s4_run_to_e2m3(ctypes.addressof(src), ctypes.addressof(out))
+    return list(out)
 
 
 def s4_run_to_fp6(run: bytes) -> list:

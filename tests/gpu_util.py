@@ -14,12 +14,15 @@ def dev(x: np.ndarray) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(x)).to("cuda")
 
 
-def gpu_gemm(dtype, A, B, variant=None, stream=None, splits=None):
+def gpu_gemm(dtype, A, B, variant=None, stream=None, splits=None, workspace=None):
     """Run the dtype's entry point (or a given variant, optionally with an
     explicit split-K count) on numpy operands; returns C as numpy (float32 or
-    int32)."""
+    int32). An explicit variant or split gets the workspace it needs
+    (allocated through PyTorch) unless one is given."""
     Ad, Bd = dev(A), dev(B)
-    C = mp.GEMM[dtype](Ad, Bd, variant=variant, stream=stream, splits=splits)
+    if workspace is None and (variant is not None or splits is not None):
+        workspace = "auto"
+    C = mp.GEMM[dtype](Ad, Bd, variant=variant, stream=stream, splits=splits, workspace=workspace)
     torch.cuda.synchronize()
     return C.cpu().numpy()
 

@@ -34,7 +34,8 @@ def test_variant_table():
         n = mp.num_variants(dt)
         assert n >= 2
         assert mp.variant_name(dt, 0).startswith("generic")
-        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny", "wide") + (("fp6pipe", "fp6wide") if dt == "s4" else ())
+        prefixes = ("tile", "pipe", "spread", "staged", "pingpong", "deep", "skinny", "wide") + \
+            (("fp6pipe", "fp6wide", "e2m3wide") if dt == "s4" else ())
         assert all(mp.variant_name(dt, v).startswith(prefixes) for v in range(1, n))
         assert mp.variant_name(dt, n) == ""
     assert mp.lib().mpgemm_num_variants(7) == -1
@@ -120,9 +121,9 @@ def test_lds_swizzle_is_a_permutation(ch):
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
-        8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6wide256x256_w2x2_k128_s3",),
-        4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("fp6wide256x256_w2x2_k128_s3",),
-        2048: ("spread128x128_w2x2_k128_s4",) * 3,
+        8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
+        4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
+        2048: ("spread128x128_w2x2_k128_s4",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
         512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
     }
@@ -193,8 +194,9 @@ def test_fp6_wide_workspace_offset_bound():
     assert not mp.variant_supports("s4", wide, 256, 65536, 1 << 17)
     assert mp.variant_supports("s4", pipe, 65536, 256, 1 << 17)
     assert mp.variant_supports("s4", wide, 16384, 256, 1 << 17)
-    assert mp.select_variant("s4", 65536, 4096, 1 << 17) == pipe
-    assert mp.select_variant("s4", 16384, 4096, 1 << 17) == wide
+    # kernels fed by the pre-pass need a workspace: never the automatic choice
+    for shape in [(65536, 4096, 1 << 17), (16384, 4096, 1 << 17), (8192, 8192, 8192), (4096, 4096, 70000)]:
+        assert not mp.variant_name("s4", mp.select_variant("s4", *shape)).startswith("fp6")
 
 
 def test_skinny_selection():
@@ -316,3 +318,132 @@ def test_wide_variant_support():
         assert not mp.variant_supports(dt, v, 256, 200, e)       # ragged N
         assert not mp.variant_supports(dt, v, 256, 256, e + 2)   # K off the slice
         assert not mp.variant_supports(dt, v, 256, 256, e, a_ptr=(1 << 20) + 4)  # unaligned A
+
+
+def _e2m3_value(c):
+    """Value of a 6-bit FP6 E2M3 code from the format's definition: sign bit 5,
+    exponent bits 4..3 with bias 1, mantissa bits 2..0, subnormals at
+    exponent 0 (OCP Microscaling Formats v1.0)."""
+    sign = -1.0 if c & 0x20 else 1.0
+    e, m = (c >> 3) & 3, c & 7
+    mag = (m / 8.0) * 2.0 ** (1 - 1) if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 1)
+    return sign * mag
+
+
+# field order of each 16 codes from a word pair (x, y): x0 y1 x3 y4 x6 y7 x1 y2
+# x4 y5 x7 y0 x2 y3 x5 y6 (nibble n of a word at bits 4n..4n+3)
+E2M3_FIELDS = [(0, 0), (1, 1), (0, 3), (1, 4), (0, 6), (1, 7), (0, 1), (1, 2),
+               (0, 4), (1, 5), (0, 7), (1, 0), (0, 2), (1, 3), (0, 5), (1, 6)]
+
+
+def test_s4_to_e2m3_encoding_is_exact():
+    """The in-GEMM INT4 conversion: every nibble v lands in exactly one of the
+    32 fields, in the documented order, as an E2M3 code whose value is
+    exactly (v + 8) / 8 (non-negative, below 2): the kernel's biased sums then
+    differ from the integer sums by 8 Sa + 8 Sb + 64 K."""
+    rng = np.random.default_rng(6)
+    runs = [bytes((2 * i) | ((2 * i + 1) << 4) for i in range(8)) * 2]  # nibbles 0..15, twice
+    runs += [rng.integers(0, 256, 16, dtype=np.uint8).tobytes() for _ in range(300)]
+    runs += [b"\x88" * 16, b"\x77" * 16, b"\x00" * 16, b"\xff" * 16]
+    for run in runs:
+        words = mp.s4_run_to_e2m3(run)
+        assert len(words) == 6
+        bits = sum(int(w) << (32 * i) for i, w in enumerate(words))
+        assert bits >> 192 == 0
+        nib = [(run[e // 2] >> (4 * (e % 2))) & 0xF for e in range(32)]  # nibble e = k offset e
+        for f in range(32):
+            p, g = divmod(f, 16)
+            which, n = E2M3_FIELDS[g]
+            k = 8 * (2 * p + which) + n  # word 2p + which, nibble n
+            v = nib[k] - 16 if nib[k] >= 8 else nib[k]
+            code = (bits >> (6 * f)) & 0x3F
+            assert _e2m3_value(code) == (v + 8) / 8.0, (run.hex(), f)
+        used = sorted(8 * (2 * (f // 16) + E2M3_FIELDS[f % 16][0]) + E2M3_FIELDS[f % 16][1] for f in range(32))
+        assert used == list(range(32))
+
+
+def test_e2m3_bias_identity_is_exact():
+    """The bias removal the kernel applies, checked on integers: with
+    u = v + 8, sum u_a u_b - 8 Sa - 8 Sb - 64 K = sum a b, and the largest
+    biased sum 225 K stays below 2^24 for every K the kernel takes."""
+    rng = np.random.default_rng(7)
+    for K in (256, 4096, 65536):
+        a = rng.integers(-8, 8, K)
+        b = rng.integers(-8, 8, K)
+        ua, ub = a + 8, b + 8
+        assert int(ua @ ub) - 8 * int(a.sum()) - 8 * int(b.sum()) - 64 * K == int(a @ b)
+        assert 225 * K < 2 ** 24
+
+
+def test_e2m3_wide_support():
+    """The INT4 kernel with the conversion inside the GEMM: K a multiple of
+    256 up to 65536 (225 K < 2^24), 16-byte aligned rows, any M and N."""
+    v = [i for i in range(mp.num_variants("s4")) if mp.variant_name("s4", i) == "e2m3wide256x256_w2x2_k256"]
+    assert len(v) == 1
+    v = v[0]
+    assert mp.variant_supports("s4", v, 256, 256, 256)
+    assert mp.variant_supports("s4", v, 300, 77, 65536)            # ragged M and N
+    assert not mp.variant_supports("s4", v, 256, 256, 65536 + 256)  # beyond the exact range
+    assert not mp.variant_supports("s4", v, 256, 256, 384)          # K off the 256 grid
+    assert not mp.variant_supports("s4", v, 256, 256, 512, a_ptr=(1 << 20) + 8)
+    for dt in ("f16", "s8"):
+        assert not any(mp.variant_name(dt, i).startswith("e2m3") for i in range(mp.num_variants(dt)))
+    # beyond its K range INT4 runs on the INT8 MFMA (K < 131072), then the bounds-checked kernel
+    assert mp.variant_name("s4", mp.select_variant("s4", 4096, 4096, 65536 + 256)).startswith("staged")
+    assert mp.select_variant("s4", 256, 256, 131072) == 0
+
+
+def test_workspace_sizes():
+    """The plain entry points' kernels need no workspace; split K needs the
+    counter block plus its partial tiles, zero points their row sums, the FP6
+    pre-pass variants their converted operands."""
+    for dt in ("f16", "s8", "s4"):
+        for n in (512, 1024, 2048, 4096, 8192):
+            assert mp.workspace_size(dt, n, n, n) == 0
+        assert mp.workspace_size(dt, 0, 5, 8) == 0
+    counters = 64 * 1024
+    # 128 rows on the small side: 128x128 tiles split 4 ways (FP16)
+    v = mp.select_variant("f16", 64, 1000, 8192)
+    sp = mp.select_splits("f16", v, 64, 1000, 8192)
+    assert sp == 4
+    assert mp.workspace_size("f16", 64, 1000, 8192) == counters + 8 * sp * 128 * 128 * 4
+    assert mp.workspace_size("f16", 64, 1000, 8192, variant=v, splits=1) == 0
+    # zero points: 4 (M + N) bytes rounded to 256, after the counter block
+    E = mp.gemm.Epilogue
+    zp = E(None, None, 1 << 20, None, 2)
+    assert mp.workspace_size("s8", 512, 512, 512, epi=zp) == counters + 4096
+    assert mp.workspace_size("s8", 100, 3, 512, epi=zp) == counters + 512
+    assert mp.workspace_size("s8", 512, 512, 512, epi=E(1 << 20, None, None, None, 2)) == 0
+    # an FP6 pre-pass variant: 0.75 byte per padded element of A and B
+    names = [mp.variant_name("s4", i) for i in range(mp.num_variants("s4"))]
+    f6 = names.index("fp6wide256x256_w2x2_k128_s3")
+    assert mp.workspace_size("s4", 1000, 300, 1000, variant=f6) == counters + (1024 + 512) * 1024 * 3 // 4
+    with pytest.raises(mp.HipError):
+        mp.workspace_size("s8", -1, 8, 8)
+    with pytest.raises(mp.HipError):
+        mp.workspace_size("f16", 256, 256, 256, epi=zp)  # zero points with FP16 inputs
+    with pytest.raises(mp.HipError):
+        mp.workspace_size("s8", 256, 256, 256, variant=0, splits=2)  # the bounds-checked kernel does not split
+
+
+def test_workspace_arguments_rejected_on_host():
+    """A misaligned workspace, one overlapping an operand, or none where the
+    call cannot do without: refused before anything is enqueued."""
+    L = mp.lib()
+    A, B, C = 1 << 20, 1 << 40, 1 << 44
+    W = 1 << 46
+    gw = lambda ws, n, M=64, N=64, K=64, epi=None: L.mpgemm_gemm_ws(1, M, N, K, A, B, C, epi, ws, n, None)
+    assert gw(W + 16, 1 << 20) == 1               # not 256-byte aligned
+    assert gw(C, 1 << 20) == 1                    # overlaps C
+    assert gw(A - 256, 1 << 20) == 1              # overlaps A
+    E = mp.gemm.Epilogue
+    zp = E(None, None, 1 << 30, None, 2)
+    import ctypes as ct
+    assert L.gemm_scaled(1, 64, 64, 64, A, B, C, ct.addressof(zp), None) == 1   # zero points need a workspace
+    assert L.mpgemm_gemm_ws(1, 64, 64, 64, A, B, C, ct.addressof(zp), W, 256, None) == 1  # too small
+    names = [mp.variant_name("s4", i) for i in range(mp.num_variants("s4"))]
+    f6 = names.index("fp6wide256x256_w2x2_k128_s3")
+    assert L.mpgemm_run_variant_ws(2, f6, 0, 256, 256, 256, A, B, C, None, None, 0, None) == 1
+    v = mp.select_variant("s8", 64, 1000, 8192)
+    assert L.mpgemm_run_variant_ws(1, v, 2, 64, 1000, 8192, A, B, C, None, None, 0, None) == 1
+    assert L.mpgemm_run_variant_ws(1, v, -1, 64, 1000, 8192, A, B, C, None, None, 0, None) == 1

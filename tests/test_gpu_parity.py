@@ -123,6 +123,11 @@ def _variant_shapes(dtype, v):
             return []
         e = {"f16": 64, "s8": 128}[dtype]
         return [(256, 256, e), (512, 768, 3 * e), (768, 256, 5 * e), (512, 512, 33 * e), (256, 1024, 2 * e)]
+    if name.startswith("e2m3"):
+        # INT4 with the conversion inside the GEMM: K a multiple of 256 (two
+        # slices per loop iteration: 1, 5 and 8 iterations), ragged M and N
+        return [(256, 256, 256), (512, 768, 1280), (300, 77, 512), (1, 255, 256), (257, 513, 768),
+                (33, 65, 2048), (768, 256, 256)]
     bm, bn = (int(x) for x in re.match(r"(?:fp6)?[a-z]+(\d+)x(\d+)_", name).groups())
     if name.startswith("fp6"):
         # INT4 on the FP6 cores: any even K (zero-padded to whole stages)
@@ -355,58 +360,184 @@ def test_two_streams():
 
 
 def _fp6_variants():
+    """Variants fed by the FP6 E3M2 conversion pre-pass (need a workspace)."""
     return [v for v in range(mp.num_variants("s4")) if mp.variant_name("s4", v).startswith("fp6")]
 
 
-def test_fp6_exact_at_the_k_limit():
-    """K = 2^18: the largest K the FP6 kernels take. All -8 sums to exactly
-    2^24 (the top of FP32's exact integer range), -8 * 7 to -56 * 2^18, and a
-    seeded random case matches the oracle bit for bit; ragged 33 x 65 tile."""
-    K = 1 << 18
-    e8 = dev(np.full((33, K // 2), 0x88, np.uint8))
-    s7 = dev(np.full((65, K // 2), 0x77, np.uint8))
-    e8b = dev(np.full((65, K // 2), 0x88, np.uint8))
-    A, B = si.gen_operands("s4", 33, 65, K, seed=2024)
-    ref = oracle.gemm_s4(A, B)
-    for v in _fp6_variants():
-        name = mp.variant_name("s4", v)
-        _log(f"fp6 K-limit {name}")
-        assert bool((mp.gemm_s4_s32(e8, e8b, variant=v) == 64 * K).all()), name
-        assert bool((mp.gemm_s4_s32(e8, s7, variant=v) == -56 * K).all()), name
-        C = gpu_gemm("s4", A, B, variant=v)
-        assert np.array_equal(C.astype(np.int64), ref), name
+def _e2m3_variants():
+    """Variants converting to biased FP6 E2M3 inside the GEMM (no workspace)."""
+    return [v for v in range(mp.num_variants("s4")) if mp.variant_name("s4", v).startswith("e2m3")]
 
 
-def test_fp6_workspace_sizes_in_one_stream():
-    """Back-to-back FP6 calls of growing and shrinking size on one stream,
-    no synchronisation between them: each call's stream-ordered workspace
-    must not disturb the others."""
+def _chunk_sums_hit_low_bits(a_vals, b_vals, bias, floor_bits):
+    """CPU check that a test pattern can expose an accumulator narrower than
+    FP32's 24 bits: the exact running sums the MFMA's FP32 accumulator holds
+    after each 64-k chunk (k-chunks of 64 consecutive k, as the kernels feed
+    them), in units of one product of biased values u = v + bias, include one
+    of magnitude >= 2^floor_bits units whose lowest bit is set. Also returns
+    whether every running sum stays below 2^24 units (the exact range)."""
+    u = (np.asarray(a_vals, np.int64) + bias) * (np.asarray(b_vals, np.int64) + bias)
+    run = np.cumsum(u.reshape(-1, 64).sum(axis=1))
+    hit = (np.abs(run) >= 2 ** floor_bits) & (run % 2 == 1)
+    return bool(hit.any()), int(run.max()) < 2 ** 24
+
+
+def _pack_rows(vals):
+    return si.pack_s4(np.asarray(vals, np.int8))
+
+
+def _adversarial_s4(K, rows_a, rows_b, seed):
+    """Three patterns per K (A rows, B rows as INT4 values), each with the
+    oracle's result:
+      ones-odd: A all 7, B all 7 except one k per 64-k chunk set to 6 (every
+        chunk adds the odd 63 * 49 + 42 = 3129);
+      mirror: the same with B negated (-7, one -6 per chunk);
+      step: A = 7 (first half of K) then -7 alternating with 7 for k odd; B = 7
+        (first half) then seeded values in [-8, 7]: the running sum climbs
+        towards the top of the exact range, then odd terms of both signs
+        arrive."""
+    half = K // 2
+    a1 = np.full(K, 7, np.int8)
+    b1 = np.full(K, 7, np.int8)
+    b1[5::64] = 6
+    rng = np.random.default_rng(seed)
+    a3 = np.full(K, 7, np.int8)
+    a3[half:] = np.where(np.arange(K - half) % 2 == 0, -7, 7)
+    b3 = np.full(K, 7, np.int8)
+    b3[half:] = rng.integers(-8, 8, K - half)
+    out = []
+    for name, av, bv in (("ones-odd", a1, b1), ("mirror", a1, -b1), ("step", a3, b3)):
+        out.append((name, av, bv, _pack_rows(np.tile(av, (rows_a, 1))), _pack_rows(np.tile(bv, (rows_b, 1)))))
+    return out
+
+
+@pytest.mark.parametrize("K", [8192, 1 << 17, 1 << 18])
+def test_fp6_prepass_exact_at_large_sums(K):
+    """The FP6 E3M2 pre-pass kernels accumulate exact integers in FP32: the
+    adversarial patterns drive the running sums to 2^20..2^23.6 with odd low
+    bits (checked on the CPU first), on every such variant, on a whole
+    256 x 256 tile and a ragged 33 x 65 one, bit-exact against the oracle."""
+    cases = _adversarial_s4(K, 256, 256, seed=K)
+    for name, av, bv, A, B in cases:
+        if K >= 1 << 17:
+            hit, fits = _chunk_sums_hit_low_bits(av, bv, 0, 20)
+            assert fits
+            assert hit, f"{name} K={K}: no odd running sum above 2^20"
+        ref = oracle.gemm_s4(A, B)
+        ref_r = ref[:33, :65]
+        for v in _fp6_variants():
+            vn = mp.variant_name("s4", v)
+            _log(f"fp6 pre-pass {vn} K={K} {name}")
+            C = gpu_gemm("s4", A, B, variant=v)
+            assert np.array_equal(C.astype(np.int64), ref), (vn, name, K)
+            C = gpu_gemm("s4", A[:33], B[:65], variant=v)
+            assert np.array_equal(C.astype(np.int64), ref_r), (vn, name, K, "ragged")
+
+
+@pytest.mark.parametrize("K", [8192, 1 << 15, 1 << 16])
+def test_e2m3_exact_at_large_sums(K):
+    """The INT4 kernel with the conversion inside the GEMM holds biased sums
+    sum (a + 8)(b + 8) / 64 in FP32: the same patterns drive them to
+    2^22..2^23.8 units of 1/64 with odd low bits (checked on the CPU), on
+    every such variant, whole tiles and ragged ones, and through gemm_s4_s32,
+    bit-exact against the oracle."""
+    cases = _adversarial_s4(K, 256, 512, seed=K + 1)
+    for name, av, bv, A, B in cases:
+        if K == 1 << 16:
+            hit, fits = _chunk_sums_hit_low_bits(av, bv, 8, 22)
+            assert fits, f"{name}: biased sum leaves the exact range"
+            # in the biased domain the mirror's products are small (u_b = 1, 2)
+            assert hit or name == "mirror", f"{name} K={K}: no odd running sum above 2^22"
+        ref = oracle.gemm_s4(A, B)
+        for v in _e2m3_variants():
+            vn = mp.variant_name("s4", v)
+            _log(f"e2m3 {vn} K={K} {name}")
+            C = gpu_gemm("s4", A, B, variant=v)
+            assert np.array_equal(C.astype(np.int64), ref), (vn, name, K)
+            C = gpu_gemm("s4", A[:33], B[:65], variant=v)
+            assert np.array_equal(C.astype(np.int64), ref[:33, :65]), (vn, name, K, "ragged")
+        C = gpu_gemm("s4", A, B)  # the entry point's own choice
+        assert np.array_equal(C.astype(np.int64), ref), (name, K, "entry point")
+
+
+def test_s4_4096_adversarial_through_the_entry_point():
+    """gemm_s4_s32 at 4096^3 on the adversarial patterns (the INT4 sweep's
+    configuration size), bit-exact."""
+    n = 4096
+    v = mp.select_variant("s4", n, n, n)
+    assert mp.variant_name("s4", v).startswith("e2m3")
+    for name, av, bv, A, B in _adversarial_s4(n, n, n, seed=44):
+        C = gpu_gemm("s4", A, B)
+        rows = np.array([0, 1, 2047, n - 1])
+        ref = oracle.gemm_s4(A, B, rows=rows)
+        assert np.array_equal(C[rows].astype(np.int64), ref), name
+        assert np.all(C == C[0, 0]), name  # identical rows of A and of B: one value
+
+
+def test_fp6_prepass_one_workspace_in_one_stream():
+    """Back-to-back FP6 pre-pass calls of growing and shrinking size on one
+    stream, no synchronisation between them, all sharing one caller
+    workspace sized for the largest (calls in order on a stream may share
+    one)."""
     v = max(_fp6_variants(), key=lambda x: mp.variant_name("s4", x).startswith("fp6pipe128"))
+    shapes = [(512, 384, 512), (2048, 1536, 1024), (256, 128, 4096), (1024, 1024, 2050)]
+    ws = mp.new_workspace(max(mp.workspace_size("s4", *sh, variant=v) for sh in shapes), "cuda")
     cases = []
-    for i, (M, N, K) in enumerate([(512, 384, 512), (2048, 1536, 1024), (256, 128, 4096), (1024, 1024, 2050)]):
+    for i, (M, N, K) in enumerate(shapes):
         A, B = si.gen_operands("s4", M, N, K, seed=300 + i)
-        cases.append((A, B, mp.gemm_s4_s32(dev(A), dev(B), variant=v)))
+        cases.append((A, B, mp.gemm_s4_s32(dev(A), dev(B), variant=v, workspace=ws)))
     torch.cuda.synchronize()
     for A, B, C in cases:
         assert np.array_equal(C.cpu().numpy().astype(np.int64), oracle.gemm_s4(A, B))
 
 
 def test_fp6_two_streams():
-    """Two FP6 INT4 GEMMs in flight on two streams at once."""
+    """Two FP6 pre-pass INT4 GEMMs in flight on two streams at once, each with
+    its own workspace; and two in-GEMM-conversion ones (no workspace)."""
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
-    v = _fp6_variants()[0]
     A1, B1 = si.gen_operands("s4", 2048, 2048, 2048, seed=51)
     A2, B2 = si.gen_operands("s4", 1024, 768, 4096, seed=52)
     d = [dev(x) for x in (A1, B1, A2, B2)]
+    for v in (_fp6_variants()[0], _e2m3_variants()[0]):
+        w1 = mp.new_workspace(mp.workspace_size("s4", 2048, 2048, 2048, variant=v), "cuda")
+        w2 = mp.new_workspace(mp.workspace_size("s4", 1024, 768, 4096, variant=v), "cuda")
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s1):
+            C1 = mp.gemm_s4_s32(d[0], d[1], stream=s1, variant=v, workspace=w1)
+        with torch.cuda.stream(s2):
+            C2 = mp.gemm_s4_s32(d[2], d[3], stream=s2, variant=v, workspace=w2)
+        s1.synchronize()
+        s2.synchronize()
+        assert np.array_equal(C1.cpu().numpy().astype(np.int64), oracle.gemm_s4(A1, B1))
+        assert np.array_equal(C2.cpu().numpy().astype(np.int64), oracle.gemm_s4(A2, B2))
+
+
+def test_s4_4096_in_a_hip_graph():
+    """gemm_s4_s32 at 4096^3 recorded into a HIP graph (it allocates, frees
+    and synchronises nothing) and replayed three times, with eager work and
+    synchronisation between the replays; every replay bit-exact."""
+    n = 4096
+    A, B = si.gen_operands("s4", n, n, n, seed=2)
+    Ad, Bd = dev(A), dev(B)
+    C = torch.empty((n, n), dtype=torch.int32, device="cuda")
+    eager = mp.gemm_s4_s32(Ad, Bd)
     torch.cuda.synchronize()
-    with torch.cuda.stream(s1):
-        C1 = mp.gemm_s4_s32(d[0], d[1], stream=s1, variant=v)
-    with torch.cuda.stream(s2):
-        C2 = mp.gemm_s4_s32(d[2], d[3], stream=s2, variant=v)
-    s1.synchronize()
-    s2.synchronize()
-    assert np.array_equal(C1.cpu().numpy().astype(np.int64), oracle.gemm_s4(A1, B1))
-    assert np.array_equal(C2.cpu().numpy().astype(np.int64), oracle.gemm_s4(A2, B2))
+    rows = np.array([0, 1, 1234, n - 1])
+    assert np.array_equal(eager.cpu().numpy()[rows].astype(np.int64), oracle.gemm_s4(A, B, rows=rows))
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        mp.gemm_s4_s32(Ad, Bd, C=C, stream=s)
+    for r in range(3):
+        C.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(C, eager), f"replay {r}"
+        junk = mp.gemm_s4_s32(Bd, Ad)  # eager work between the replays
+        torch.cuda.synchronize()
+        del junk
 
 
 # ---------------------------------------------------------------- split-K and LLM-inference shapes
@@ -420,7 +551,8 @@ def _pipelined_variants(dtype):
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_splitk_every_pipelined_variant(dtype):
     """Every split-capable variant with 2, 3 and 4 K-ranges on ragged shapes
-    spanning several tiles: bit-exact integers, FP16 within the bound."""
+    spanning several tiles (caller workspaces): bit-exact integers, FP16
+    within the bound."""
     for v in _pipelined_variants(dtype):
         name = mp.variant_name(dtype, v)
         bm, bn = (int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
@@ -437,15 +569,18 @@ def test_splitk_every_pipelined_variant(dtype):
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_llm_inference_shapes(dtype):
     """Skinny GEMMs of LLM inference (M tokens x N outputs x K inputs) through
-    the entry point, whatever kernel and split it picks."""
+    the entry point (no workspace: never split) and through mpgemm_gemm_ws
+    with a workspace (split where the choice splits), whatever kernel it
+    picks."""
     for (M, N, K) in [(1, 4096, 4096), (16, 4096, 4096), (64, 8192, 4096), (128, 4096, 8192),
                       (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048),
                       # the narrow tiles, mirrored when N is the small side
                       (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
-        C = gpu_gemm(dtype, A, B)
+        ref = oracle_gemm(dtype, A, B)
         v = mp.select_variant(dtype, M, N, K)
-        assert_parity(dtype, C, *oracle_gemm(dtype, A, B),
+        assert_parity(dtype, gpu_gemm(dtype, A, B), *ref, f"{dtype} {M}x{N}x{K} {mp.variant_name(dtype, v)}")
+        assert_parity(dtype, gpu_gemm(dtype, A, B, workspace="auto"), *ref,
                       f"{dtype} {M}x{N}x{K} {mp.variant_name(dtype, v)} splits {mp.select_splits(dtype, v, M, N, K)}")
     _log(f"{dtype} LLM shapes: ok")
 
@@ -453,24 +588,29 @@ def test_llm_inference_shapes(dtype):
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_splitk_deterministic_and_concurrent(dtype):
     """Split results do not depend on which workgroup finishes last (five
-    launches bit-identical), and two split-K GEMMs on two streams at once
-    keep separate workspaces."""
+    launches on one reused workspace bit-identical: each call leaves its
+    counters zero), and two split-K GEMMs on two streams at once, each with
+    its own workspace."""
     v = [x for x in _pipelined_variants(dtype) if mp.variant_name(dtype, x) == "spread128x128_w2x2_k64_s4"][0]
     A, B = si.gen_operands(dtype, 512, 640, 2048, seed=91)
     Ad, Bd = dev(A), dev(B)
-    first = mp.GEMM[dtype](Ad, Bd, variant=v, splits=8)
+    ws = mp.new_workspace(mp.workspace_size(dtype, 512, 640, 2048, variant=v, splits=8), "cuda")
+    first = mp.GEMM[dtype](Ad, Bd, variant=v, splits=8, workspace=ws)
     for _ in range(4):
-        assert torch.equal(first, mp.GEMM[dtype](Ad, Bd, variant=v, splits=8))
+        assert torch.equal(first, mp.GEMM[dtype](Ad, Bd, variant=v, splits=8, workspace=ws))
     torch.cuda.synchronize()
     assert_parity(dtype, first.cpu().numpy(), *oracle_gemm(dtype, A, B), f"{dtype} split 8")
     A2, B2 = si.gen_operands(dtype, 384, 256, 4096, seed=92)
     A2d, B2d = dev(A2), dev(B2)
     s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
     torch.cuda.synchronize()
+    w1 = mp.new_workspace(mp.workspace_size(dtype, 512, 640, 2048, variant=v, splits=4), "cuda")
+    w2 = mp.new_workspace(mp.workspace_size(dtype, 384, 256, 4096, variant=v, splits=16), "cuda")
+    torch.cuda.synchronize()
     with torch.cuda.stream(s1):
-        C1 = mp.GEMM[dtype](Ad, Bd, variant=v, splits=4, stream=s1)
+        C1 = mp.GEMM[dtype](Ad, Bd, variant=v, splits=4, stream=s1, workspace=w1)
     with torch.cuda.stream(s2):
-        C2 = mp.GEMM[dtype](A2d, B2d, variant=v, splits=16, stream=s2)
+        C2 = mp.GEMM[dtype](A2d, B2d, variant=v, splits=16, stream=s2, workspace=w2)
     s1.synchronize()
     s2.synchronize()
     assert_parity(dtype, C1.cpu().numpy(), *oracle_gemm(dtype, A, B), f"{dtype} stream 1")
@@ -482,12 +622,15 @@ def test_splitk_argument_errors():
     t = torch.zeros((256, 1024), dtype=torch.int8, device="cuda")
     L = mp.lib()
     c = torch.zeros((256, 256), dtype=torch.int32, device="cuda")
-    run = lambda var, sp, K: L.mpgemm_run_variant_splits(1, var, sp, 256, 256, K, t.data_ptr(), t.data_ptr(),
-                                                         c.data_ptr(), 0)
-    assert run(v, 0, 1024) == INVALID
+    ws = mp.new_workspace(mp.workspace_size("s8", 256, 256, 1024, variant=v, splits=16), "cuda")
+    run = lambda var, sp, K, w=ws.data_ptr(), n=ws.numel(): L.mpgemm_run_variant_ws(
+        1, var, sp, 256, 256, K, t.data_ptr(), t.data_ptr(), c.data_ptr(), None, w, n, 0)
+    assert run(v, -1, 1024) == INVALID
     assert run(v, 17, 1024) == INVALID
     assert run(v, 3, 1024) == INVALID  # 16 slices do not split in 3
     assert run(0, 2, 1024) == INVALID  # the bounds-checked kernel does not split
+    assert run(v, 16, 1024, None, 0) == INVALID  # a split needs a workspace
+    assert run(v, 16, 1024, ws.data_ptr(), 4096) == INVALID  # too small for it
     assert run(v, 16, 1024) == 0
     torch.cuda.synchronize()
 
@@ -515,8 +658,9 @@ def _scales(dtype, M, N, seed, zero_points):
 
 def _run_scaled(dtype, A, B, out, sa, sb, za, zb, variant=None, splits=None):
     t = lambda x: None if x is None else dev(x)
+    ws = "auto" if (variant is not None or za is not None or zb is not None) else None
     C = mp.gemm_scaled(dtype, dev(A), dev(B), t(sa), t(sb), t(za), t(zb), out_dtype=TORCH_OUT[out],
-                       variant=variant, splits=splits)
+                       variant=variant, splits=splits, workspace=ws)
     torch.cuda.synchronize()
     return C
 
@@ -576,7 +720,12 @@ def test_scaled_argument_errors():
     assert call(1, t, E(s.data_ptr() + 2, None, None, None, 2)) == INVALID  # misaligned scales
     assert call(1, t, E(None, None, None, None, 1), c.data_ptr() + 2) == INVALID  # FP32 output: 4-byte C
     assert call(1, t, E(None, None, None, None, 2), c.data_ptr() + 1) == INVALID  # FP16 output: 2-byte C
-    assert call(1, t, E(s.data_ptr(), s.data_ptr(), z.data_ptr(), z.data_ptr(), 3)) == 0
+    assert call(1, t, E(None, None, z.data_ptr(), None, 2)) == INVALID      # zero points need a workspace
+    assert call(1, t, E(s.data_ptr(), s.data_ptr(), None, None, 3)) == 0
+    ws = mp.new_workspace(1 << 17, "cuda")
+    epi = E(s.data_ptr(), s.data_ptr(), z.data_ptr(), z.data_ptr(), 3)
+    assert L.mpgemm_gemm_ws(1, 64, 64, 64, t.data_ptr(), t.data_ptr(), c.data_ptr(), ctypes.addressof(epi),
+                            ws.data_ptr(), ws.numel(), 0) == 0
     torch.cuda.synchronize()
 
 
