@@ -52,6 +52,8 @@ PEAK_UNIT = {"f16": "TFLOP/s", "s8": "TOP/s", "s4": "TOP/s"}
 IN_BYTES = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 METRIC = "TFLOP/s | TOP/s at N=512–8192 for FP16, INT8, INT4; % of MFMA peak per dtype"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# precisions timed through mpgemm_gemm_ws with a workspace
+WS_DTYPES = ("s4",)
 # rows of each N = 8192 point the CPU oracle computes for the baseline sample
 CPU_SAMPLE_ROWS = {"f16": 1024, "s8": 8192, "s4": 8192}
 
@@ -171,12 +173,16 @@ def main():
         Bd = torch.from_numpy(B).to(dev)
         C = torch.empty((n, n), dtype=torch.float32 if dt == "f16" else torch.int32, device=dev)
         v = forced.get((dt, n))
-        vsel = v if v is not None else mp.select_variant(dt, n, n, n, Ad.data_ptr(), Bd.data_ptr(),
-                                                         C.data_ptr())
-        # the default choice needs no workspace; a forced variant may (split K,
-        # FP6 pre-pass): allocated here, before timing
-        wsb = mp.workspace_size(dt, n, n, n, variant=v)
+        # INT4 goes through mpgemm_gemm_ws with a workspace (allocated here,
+        # before timing), which takes the FP6 kernel fed by the conversion
+        # pre-pass where that is faster; FP16 and INT8 through their plain
+        # entry points (no workspace); a forced variant gets the workspace it
+        # needs
+        use_ws = dt in WS_DTYPES or v is not None
+        wsb = mp.workspace_size(dt, n, n, n, variant=v) if use_ws else 0
         ws = mp.new_workspace(wsb, dev) if wsb else None
+        vsel = v if v is not None else mp.select_variant(dt, n, n, n, Ad.data_ptr(), Bd.data_ptr(),
+                                                         C.data_ptr(), with_ws=ws is not None)
         bufs.append(dict(dt=dt, n=n, seed=seed, A=Ad, B=Bd, C=C, host=(A, B), variant=v,
                          vname=mp.variant_name(dt, vsel), ws=ws, ws_bytes=wsb))
     torch.cuda.synchronize()
@@ -276,8 +282,8 @@ def main():
                         if args.points == "sweep" else f"points {args.points}",
             "points": len(bufs),
             "ops_per_step": total_ops,
-            "entry_points": "gemm_f16_f32, gemm_s8_s32, gemm_s4_s32 (no workspace)"
-                            if not forced else "forced variants via mpgemm_run_variant(_ws)",
+            "entry_points": "FP16 gemm_f16_f32, INT8 gemm_s8_s32 (no workspace); INT4 mpgemm_gemm_ws "
+                            "with a caller workspace" if not forced else "forced variants via mpgemm_run_variant(_ws)",
             "workspace_bytes": int(sum(b["ws_bytes"] for b in bufs)),
         },
         "clock_mhz": clock_mhz,
@@ -291,7 +297,7 @@ def main():
 
 class ClockSampler:
     """Samples the GPU shader clock the driver reports (the active level of
-    pp_dpm_sclk in sysfs) every 20 ms on a host thread; stop() returns the
+    pp_dpm_sclk in sysfs) every 5 ms on a host thread; stop() returns the
     median, min and max in MHz, or None where the file is not readable."""
 
     def __init__(self):
@@ -316,7 +322,7 @@ class ClockSampler:
             v = self._read()
             if v is not None:
                 self.samples.append(v)
-            time.sleep(0.02)
+            time.sleep(0.005)
 
     def start(self):
         import threading

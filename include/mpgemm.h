@@ -202,6 +202,12 @@ const char *mpgemm_variant_name(int dtype, int variant);
 int mpgemm_select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
                           const void *C);
 
+/* The variant mpgemm_gemm_ws runs for these arguments with a workspace that
+ * holds that variant's scratch (INT4 then takes the FP6 kernels fed by the
+ * conversion pre-pass where they are faster), or -1 for invalid arguments. */
+int mpgemm_select_variant_ws(int dtype, int M, int N, int K, const void *A, const void *B,
+                             const void *C);
+
 /* Whether `variant` can run these arguments: 1 yes, 0 no, -1 invalid dtype. */
 int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const void *A,
                             const void *B, const void *C);

@@ -191,18 +191,27 @@ enum : int {
     V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
 };
 // INT4-only variants follow the common list in kS4.
-constexpr int V_I4WIDE = kNumCommon + 9;   // e2m3wide256x256_w2x2_k256
+constexpr int V_FP6_256_S2 = kNumCommon + 1;  // fp6pipe256x256_w2x4_k128_s2
+constexpr int V_FP6_WIDE = kNumCommon + 8;    // fp6wide256x256_w2x2_k128_s3
+constexpr int V_I4WIDE = kNumCommon + 9;      // e2m3wide256x256_w2x2_k256
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
 // taken when it supports the problem and yields at least `min_tiles`
 // workgroups (256 = one per CU). Chosen from interleaved timings of every
 // variant at N = 512 ... 8192 on MI355X.
 struct Pref { int variant; long min_tiles; };
-// INT4: the FP6 kernel with the conversion inside the GEMM (no pre-pass, no
-// workspace) from 64 tiles of 256 x 256 (N = 2048 square); below that, or
-// for K beyond its exact range or off its 256-k grid, the INT8-MFMA kernels.
-// The FP6 kernels fed by a conversion pre-pass need a workspace and are
-// never chosen automatically.
+// INT4 without a workspace: the FP6 kernel with the conversion inside the
+// GEMM (no pre-pass, no workspace) once 256 x 256 tiles fill the CUs (at
+// 8192^3 415-455 us against 478 us for the INT8-MFMA kernels; at 2048^3 with
+// 64 tiles it takes 36 us against 21 us for the 128 x 128 INT8-MFMA kernel);
+// below that, or for K beyond its exact range or off its 256-k grid, the
+// INT8-MFMA kernels.
+// INT4 with a workspace large enough for the converted operands: the
+// one-wave-per-SIMD FP6 kernel fed by the conversion pre-pass first (at
+// 8192^3: 483k + 100k cycles per XCD for kernel and pre-pass, against 911k
+// for the in-GEMM conversion, whose 16-half-line register loads and
+// conversion do not overlap the MFMAs), then the 8-wave one where the first's
+// 32-bit workspace offsets do not reach.
 // FP16, INT8: below 256 tiles of 256 x 256 the 128-byte-slice 128 x 128
 // kernel (as fast or faster than the 64-byte one at every measured size:
 // square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
@@ -213,8 +222,10 @@ struct Pref { int variant; long min_tiles; };
 // predicated edges, where M or N is not a multiple of 256.
 const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_I4WIDE, 64}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1},
+const Pref kPrefS4[] = {{V_I4WIDE, 256}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1},
                         {V_PIPE64, 1}};
+const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 256}, {V_FP6_256_S2, 512}, {V_I4WIDE, 256}, {V_STAGED256_W2X4, 256},
+                          {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the
 // narrow tiles below (measured on MI355X at 1..32 x {4096, 8192, 14336,
@@ -288,7 +299,10 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
     return cands[best];
 }
 
-int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
+// with_ws: the choice for a call that has a workspace (INT4 may then take
+// the FP6 kernels fed by the conversion pre-pass).
+int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C,
+                   bool with_ws = false) {
     const Variant *t = table(dtype);
     const int sk = select_skinny(dtype, M, N, K, A, B, C);
     if (sk >= 0) return sk;
@@ -302,10 +316,12 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         for (int cand : {V_SPREAD128_K128, V_SPREAD128_K64})
             if (supports(dtype, t[cand], M, N, K, A, B, C)) return cand;
     }
-    const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : kPrefS4);
+    const bool s4ws = dtype == S4 && with_ws;
+    const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : (s4ws ? kPrefS4Ws : kPrefS4));
     const int n = dtype == F16 ? (int)(sizeof(kPrefF16) / sizeof(Pref))
                                : (dtype == S8 ? (int)(sizeof(kPrefS8) / sizeof(Pref))
-                                              : (int)(sizeof(kPrefS4) / sizeof(Pref)));
+                                              : (s4ws ? (int)(sizeof(kPrefS4Ws) / sizeof(Pref))
+                                                      : (int)(sizeof(kPrefS4) / sizeof(Pref))));
     for (int i = 0; i < n; ++i) {
         const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
@@ -468,7 +484,14 @@ struct Choice {
 hipError_t choose(int dtype, int variant, int splits, int M, int N, int K, const void *A, const void *B,
                   const void *C, bool zero_points, size_t ws_bytes, Choice &out) {
     const Variant *t = table(dtype);
-    if (variant < 0) variant = select_variant(dtype, M, N, K, A, B, C);
+    if (variant < 0) {
+        // the choice with a workspace where it holds that choice's scratch
+        // (the FP6 pre-pass operands; split K is decided below), else the
+        // choice without one
+        variant = select_variant(dtype, M, N, K, A, B, C, ws_bytes > 0);
+        if (ws_plan(t[variant], 1, M, N, K, zero_points).total > ws_bytes)
+            variant = select_variant(dtype, M, N, K, A, B, C, false);
+    }
     if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
     if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
     if (splits < 0) {
@@ -605,6 +628,12 @@ int mpgemm_select_variant(int dtype, int M, int N, int K, const void *A, const v
                           const void *C) {
     if (!valid_args(dtype, M, N, K, A, B, C)) return -1;
     return select_variant(dtype, M, N, K, A, B, C);
+}
+
+int mpgemm_select_variant_ws(int dtype, int M, int N, int K, const void *A, const void *B,
+                             const void *C) {
+    if (!valid_args(dtype, M, N, K, A, B, C)) return -1;
+    return select_variant(dtype, M, N, K, A, B, C, true);
 }
 
 int mpgemm_variant_supports(int dtype, int variant, int M, int N, int K, const void *A,

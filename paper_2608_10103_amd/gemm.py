@@ -59,6 +59,8 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_variant_name.restype = ctypes.c_char_p
     L.mpgemm_select_variant.argtypes = [I, I, I, I, P, P, P]
     L.mpgemm_select_variant.restype = I
+    L.mpgemm_select_variant_ws.argtypes = [I, I, I, I, P, P, P]
+    L.mpgemm_select_variant_ws.restype = I
     L.mpgemm_variant_supports.argtypes = [I, I, I, I, I, P, P, P]
     L.mpgemm_variant_supports.restype = I
     L.mpgemm_run_variant.argtypes = [I, I, I, I, I, P, P, P, P]
@@ -86,7 +88,8 @@ def lib() -> ctypes.CDLL:
 
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "gemm_scaled", "mpgemm_gemm_ws",
                     "mpgemm_workspace_size", "mpgemm_num_variants", "mpgemm_variant_name",
-                    "mpgemm_select_variant", "mpgemm_variant_supports", "mpgemm_run_variant",
+                    "mpgemm_select_variant", "mpgemm_select_variant_ws", "mpgemm_variant_supports",
+                    "mpgemm_run_variant",
                     "mpgemm_select_splits", "mpgemm_run_variant_ws", "mpgemm_s4_run_to_fp6",
                     "mpgemm_s4_run_to_e2m3", "mpgemm_gemm_bt")
 
@@ -319,16 +322,18 @@ def variant_name(dtype: str, variant: int) -> str:
 
 
 def select_variant(dtype: str, M: int, N: int, K: int, a_ptr: int = 0, b_ptr: int = 0,
-                   c_ptr: int = 16) -> int:
-    """Variant the entry point would run (pointers only matter for alignment;
-    the defaults are 16-byte aligned stand-ins, never dereferenced)."""
+                   c_ptr: int = 16, with_ws: bool = False) -> int:
+    """Variant the entry point would run (with_ws: mpgemm_gemm_ws with a large
+    enough workspace); pointers only matter for alignment, the defaults are
+    16-byte aligned stand-ins, never dereferenced."""
     if a_ptr == 0:
         a_ptr = 1 << 20
     if b_ptr == 0:
         b_ptr = 1 << 40
     if c_ptr == 16:
         c_ptr = 1 << 44
-    return lib().mpgemm_select_variant(DTYPE_CODE[dtype], M, N, K, a_ptr, b_ptr, c_ptr)
+    fn = lib().mpgemm_select_variant_ws if with_ws else lib().mpgemm_select_variant
+    return fn(DTYPE_CODE[dtype], M, N, K, a_ptr, b_ptr, c_ptr)
 
 
 def variant_supports(dtype: str, variant: int, M: int, N: int, K: int, a_ptr: int = 1 << 20,

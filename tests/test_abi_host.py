@@ -123,13 +123,20 @@ def test_selection_at_sweep_sizes():
     want = {
         8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
-        2048: ("spread128x128_w2x2_k128_s4",) * 2 + ("e2m3wide256x256_w2x2_k256",),
+        2048: ("spread128x128_w2x2_k128_s4",) * 3,
         1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
         512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
     }
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
         assert got == names, (n, got)
+    # with a workspace INT4 takes the FP6 kernel fed by the conversion pre-pass
+    for n in (4096, 8192):
+        assert mp.variant_name("s4", mp.select_variant("s4", n, n, n, with_ws=True)) == "fp6wide256x256_w2x2_k128_s3"
+        for d in ("f16", "s8"):
+            assert mp.select_variant(d, n, n, n, with_ws=True) == mp.select_variant(d, n, n, n)
+    for n in (512, 1024, 2048):
+        assert mp.select_variant("s4", n, n, n, with_ws=True) == mp.select_variant("s4", n, n, n)
     # FP16 off whole 256 x 256 tiles: the 8-wave kernel with predicated edges
     assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "pipe256x256_w2x4_k128_s2"
 
@@ -397,11 +404,14 @@ def test_workspace_sizes():
     """The plain entry points' kernels need no workspace; split K needs the
     counter block plus its partial tiles, zero points their row sums, the FP6
     pre-pass variants their converted operands."""
+    counters = 64 * 1024
     for dt in ("f16", "s8", "s4"):
         for n in (512, 1024, 2048, 4096, 8192):
-            assert mp.workspace_size(dt, n, n, n) == 0
+            want = counters + 2 * n * n * 3 // 4 if (dt == "s4" and n >= 4096) else 0  # FP6 pre-pass operands
+            assert mp.workspace_size(dt, n, n, n) == want, (dt, n)
+            if dt == "s4" and n >= 4096:  # the workspace-free choice of the plain entry point needs none
+                assert mp.workspace_size(dt, n, n, n, variant=mp.select_variant(dt, n, n, n)) == 0
         assert mp.workspace_size(dt, 0, 5, 8) == 0
-    counters = 64 * 1024
     # 128 rows on the small side: 128x128 tiles split 4 ways (FP16)
     v = mp.select_variant("f16", 64, 1000, 8192)
     sp = mp.select_splits("f16", v, 64, 1000, 8192)
