@@ -170,6 +170,22 @@ hipError_t mpgemm_gemm_ws(int dtype, int M, int N, int K, const void *A, const v
                           const mpgemm_epilogue *epi, void *workspace, size_t workspace_bytes,
                           hipStream_t stream);
 
+/* For callers that cannot allocate (code under graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): mpgemm_gemm_ws with the scratch
+ * taken from a 32 MiB array the library holds on each device it runs on
+ * (allocated with the code object, kept until the process ends) instead of
+ * a caller workspace. Allocates and frees nothing. The first call on a
+ * device looks up that device's array address (hipGetSymbolAddress). The
+ * automatic choice is the one mpgemm_gemm_ws makes with a 32 MiB workspace: a
+ * split that would need more is not taken; zero points needing more
+ * (M + N above about 8.4 million) return hipErrorInvalidValue. A split call
+ * first clears the tile counters with a small kernel on `stream`. Every
+ * call on a device shares that device's array: calls that may overlap on
+ * one device (other streams, other threads) race, and must be ordered by
+ * the caller (one stream, or events). Other arguments, semantics and errors
+ * as mpgemm_gemm_ws. */
+hipError_t mpgemm_gemm_noalloc(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                               const mpgemm_epilogue *epi, hipStream_t stream);
 
 /* B stored K x N ROW-major (B(k,j) at element k*N + j, N-contiguous): the
  * "transposed B" operand layout of the paper's INT4 ablation (Table XII),

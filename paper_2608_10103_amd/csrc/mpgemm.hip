@@ -11,6 +11,8 @@
 #include <limits.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "mpgemm.h"
 #include "variants.hpp"
 
@@ -541,6 +543,41 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
     return launch(dtype, table(dtype)[ch.variant], ch.splits, M, N, K, A, B, C, epi, ch.plan, ws, stream);
 }
 
+// ---- scratch for callers that cannot allocate (mpgemm_gemm_noalloc) ----
+// A file-scope device array: each GPU the library runs on holds its own copy
+// until the process ends. Host code must not use the name as an address (it
+// is a host-side stand-in): the device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+static_assert(kStaticScratchBytes % kWsAlign == 0, "whole workspace granules");
+__device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+hipError_t static_scratch(uint8_t **out) {
+    static std::mutex mu;
+    static uint8_t *ptr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        ptr[dev] = static_cast<uint8_t *>(p);
+    }
+    *out = ptr[dev];
+    return hipSuccess;
+}
+
+// Fill kernel for the counter block of a reused scratch (a kernel rather than
+// hipMemsetAsync, so the call can also be recorded into a graph).
+__global__ void zero_words(uint32_t *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
+}
+
 }  // namespace
 
 extern "C" {
@@ -614,6 +651,42 @@ hipError_t mpgemm_workspace_size(int dtype, int variant, int splits, int M, int 
     if (e != hipSuccess) return e;
     *bytes = ch.plan.total;
     return hipSuccess;
+}
+
+hipError_t mpgemm_gemm_noalloc(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
+                               const mpgemm_epilogue *epi, hipStream_t stream) {
+    // the checks of mpgemm_gemm_ws first: nothing is looked up or enqueued
+    // for arguments it would refuse
+    int c_elem = 4;
+    if (epi) {
+        if (dtype < F16 || dtype > S4 || !valid_epilogue(dtype, epi)) return hipErrorInvalidValue;
+        c_elem = epi->out_type == MPGEMM_OUT_F32 ? 4 : 2;
+    }
+    if (!valid_args(dtype, M, N, K, A, B, C, c_elem)) return hipErrorInvalidValue;
+    if (M == 0 || N == 0) return hipSuccess;
+    // the choice with a workspace of the scratch's size: a split that does
+    // not fit is not taken; scratch the call cannot do without (zero points
+    // beyond it) is refused
+    Choice ch;
+    const bool zp = epi && (epi->zero_a || epi->zero_b);
+    hipError_t e = choose(dtype, -1, -1, M, N, K, A, B, C, zp, kStaticScratchBytes, ch);
+    if (e != hipSuccess) return e;
+    if (ch.plan.total > kStaticScratchBytes) return hipErrorInvalidValue;
+    uint8_t *ws = nullptr;
+    if (ch.plan.total) {
+        e = static_scratch(&ws);
+        if (e != hipSuccess) return e;
+    }
+    if (ch.splits > 1) {
+        // the array keeps the last call's contents: clear the tile counters
+        uint32_t *words = reinterpret_cast<uint32_t *>(ws);
+        int n = (int)tile_count(table(dtype)[ch.variant], M, N);
+        void *args[] = {&words, &n};
+        e = hipLaunchKernel(reinterpret_cast<const void *>(&zero_words), dim3((n + 255) / 256), dim3(256), args,
+                            0, stream);
+        if (e != hipSuccess) return e;
+    }
+    return run(dtype, ch.variant, ch.splits, M, N, K, A, B, C, stream, epi, Ws{ws, ch.plan.total ? kStaticScratchBytes : 0});
 }
 
 int mpgemm_num_variants(int dtype) { return num_variants(dtype); }

@@ -72,6 +72,8 @@ def lib() -> ctypes.CDLL:
     S = ctypes.c_size_t
     L.mpgemm_gemm_ws.argtypes = [I, I, I, I, P, P, P, P, P, S, P]
     L.mpgemm_gemm_ws.restype = I
+    L.mpgemm_gemm_noalloc.argtypes = [I, I, I, I, P, P, P, P, P]
+    L.mpgemm_gemm_noalloc.restype = I
     L.mpgemm_run_variant_ws.argtypes = [I, I, I, I, I, I, P, P, P, P, P, S, P]
     L.mpgemm_run_variant_ws.restype = I
     L.mpgemm_workspace_size.argtypes = [I, I, I, I, I, I, P, ctypes.POINTER(S)]
@@ -87,6 +89,7 @@ def lib() -> ctypes.CDLL:
 
 
 EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "gemm_scaled", "mpgemm_gemm_ws",
+                    "mpgemm_gemm_noalloc",
                     "mpgemm_workspace_size", "mpgemm_num_variants", "mpgemm_variant_name",
                     "mpgemm_select_variant", "mpgemm_select_variant_ws", "mpgemm_variant_supports",
                     "mpgemm_run_variant",
