@@ -191,13 +191,16 @@ hipError_t mpgemm_gemm_noalloc(int dtype, int M, int N, int K, const void *A, co
  * "transposed B" operand layout of the paper's INT4 ablation (Table XII),
  * which cost its kernels 3x through uncoalesced loads. Here B is copied to
  * LDS as stored and turned into MFMA operands by the LDS transpose reads of
- * gfx950. dtype 0 (FP16 -> FP32 C) or 1 (INT8 -> INT32 C); A row-major M x K
- * and C row-major M x N as for the plain entry points; same semantics,
- * ownership, stream and tolerance rules.
+ * gfx950. dtype 0 (FP16 -> FP32 C), 1 (INT8 -> INT32 C) or 2 (INT4 -> INT32
+ * C; B's nibbles packed two per byte along N, the low nibble holding the even
+ * column: B(k,j) in byte k*N/2 + j/2); A row-major M x K and C row-major
+ * M x N as for the plain entry points; same semantics, ownership, stream and
+ * tolerance rules.
  * Requirements (else hipErrorInvalidValue, nothing enqueued): N a multiple
- * of 256; K a multiple of 64 (FP16) or 128 (INT8), or K == 0 (C zero-filled);
- * A and B 16-byte aligned, C 4-byte aligned; the checks of the plain entry
- * points (sizes, NULL pointers, overlap). M may be any size. No workspace. */
+ * of 256; K a multiple of 64 (FP16), 128 (INT8) or 256 (INT4, and below
+ * 131072), or K == 0 (C zero-filled); A and B 16-byte aligned, C 4-byte
+ * aligned; the checks of the plain entry points (sizes, NULL pointers,
+ * overlap). M may be any size. No workspace. */
 hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
                           hipStream_t stream);
 

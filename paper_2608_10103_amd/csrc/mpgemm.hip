@@ -584,7 +584,7 @@ extern "C" {
 
 hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const void *B, void *C,
                           hipStream_t stream) {
-    if (dtype != F16 && dtype != S8) return hipErrorInvalidValue;
+    if (dtype != F16 && dtype != S8 && dtype != S4) return hipErrorInvalidValue;
     // the size, pointer and overlap checks of the plain entry points (B
     // occupies K * N elements either way)
     if (!valid_args(dtype, M, N, K, A, B, C)) return hipErrorInvalidValue;
@@ -594,6 +594,7 @@ hipError_t mpgemm_gemm_bt(int dtype, int M, int N, int K, const void *A, const v
     const long kb = row_bytes(dtype, K);
     if (N % T::BN || kb % T::BKB || !aligned(A, 16) || !aligned(B, 16)) return hipErrorInvalidValue;
     if (kb > INT_MAX || (long)K * N > (long)INT_MAX * 16) return hipErrorInvalidValue;
+    if (dtype == S4 && K >= 131072) return hipErrorInvalidValue;  // INT4 sums carried times 256
     const uint8_t *a = static_cast<const uint8_t *>(A), *b = static_cast<const uint8_t *>(B);
     int kbi = (int)kb, tiles_m = (M + T::BM - 1) / T::BM, tiles_n = N / T::BN;
     EpiParams epi = plain_epilogue(K);

@@ -5,19 +5,25 @@
 // Here B is copied into LDS exactly as it lies in memory (whole K-rows of
 // N-contiguous bytes, the same 16-byte direct-to-LDS loads as A), and the
 // MFMA operand, which wants K-contiguous runs per column, is assembled by the
-// LDS transpose reads of gfx950 (ds_read_b64_tr_b16 / _b8). Measured lane
-// layout of those reads, per group of 16 lanes: lanes 4e..4e+3 (b16) or
-// 2e, 2e+1 (b8) supply row e (16 consecutive elements, 8 bytes per lane);
-// output lane i receives element i of every row, i.e. 4 (b16) or 8 (b8)
-// elements of column i along the row index. With the rows being consecutive
-// k of one 16-column slice, each lane gets consecutive k of its own column:
-// the MFMA operand run, two reads per 32-column block per K-chunk.
+// LDS transpose reads of gfx950 (ds_read_b64_tr_b16 / _b8 / _b4). Measured
+// lane layout of those reads, per group of 16 lanes: lanes 4e..4e+3 (b16),
+// 2e, 2e+1 (b8) or e (b4) supply row e (16 consecutive elements, 8 bytes per
+// lane); output lane i receives element i of every row, i.e. 4 (b16), 8 (b8)
+// or 16 (b4, row e in nibble e) elements of column i along the row index.
+// With the rows being consecutive k of one 16-column slice, each lane gets
+// consecutive k of its own column: the MFMA operand run, two reads per
+// 32-column block per K-chunk. For INT4 (B's nibbles packed along N, the
+// low nibble holding the even column) the two reads give 32 consecutive k
+// packed two per byte with the low nibble holding the even k, the layout of
+// a column-major INT4 run, so the decode and MFMAs are the column-major
+// kernel's.
 //
 // Everything else is the 8-wave pipelined kernel of tiled_gemm.hpp: 256 x 256
 // tile, 2 x 4 waves of 128 x 64, 128-byte K-slices of A (BKB / es k-rows of
 // B) in a 2-stage ring, operand runs double-buffered in registers, the
-// barrier inside the last K-chunk. FP16 and INT8. N must fill whole tiles
-// (the copy takes whole B rows of the tile), K whole slices; M may be ragged.
+// barrier inside the last K-chunk. FP16, INT8 and INT4. N must fill whole
+// tiles (the copy takes whole B rows of the tile), K whole slices; M may be
+// ragged.
 #pragma once
 
 #include "tiled_gemm.hpp"
@@ -26,16 +32,17 @@ namespace mpg {
 
 template <int DT, class T>
 struct TB {
-    static_assert(DT == F16 || DT == S8, "transposed B: FP16 and INT8");
     static_assert(T::MS == 32 && T::BKB == 128 && T::STAGES == 2, "the 128-byte 2-stage pipelined tile");
-    static constexpr int ES = DT == F16 ? 2 : 1;         // bytes per element
-    static constexpr int BK = T::BKB / ES;               // k per slice = B rows per stage
-    static constexpr int RB = T::BN * ES;                // bytes of one B row in the tile
+    static constexpr int EPB2 = DT == F16 ? 1 : (DT == S8 ? 2 : 4);  // elements per 2 bytes
+    static constexpr int BK = T::BKB * EPB2 / 2;         // k per slice = B rows per stage
+    static constexpr int RB = T::BN * 2 / EPB2;          // bytes of one B row in the tile
     static constexpr int CHB = RB / 16;                  // 16-byte chunks per B row
     static constexpr int ROWS_PER_UNIT = 1024 / RB;      // B rows one 1 KiB copy fills
     static constexpr int A_UNITS = T::BM * T::BKB / 1024;
-    static constexpr int RR = DT == F16 ? 4 : 8;         // B rows per transpose read
+    static constexpr int RR = 4 * EPB2;                  // B rows per transpose read: 4, 8, 16
     static constexpr int LPR = 16 / RR;                  // lanes per row in a 16-lane group
+    // byte offset of column j within a B row
+    static __host__ __device__ constexpr long col_bytes(long j) { return j * 2 / EPB2; }
     static_assert(A_UNITS % T::DMA_PER_WAVE == 0, "a wave copies only A or only B");
     static_assert(BK * RB == T::BN * T::BKB, "B part of a stage is as large as the column-major one");
 };
@@ -46,9 +53,13 @@ struct TB {
 // bytes all start on the same bank, so the chunks are spread by row: the two
 // 16-lane groups that read one 32-column block hit 16 distinct 16-byte bank
 // groups.
+// INT4: rows of 128 bytes, a read's 16 lanes take 16 consecutive rows of one
+// 8-byte column group; rows r and r + 1 start on opposite halves of the
+// 256-byte bank row, so slot (r / 2) % 8 spreads the 16 rows over 16 distinct
+// 8-byte bank pairs.
 template <int DT>
 __host__ __device__ constexpr int tb_swz(int r) {
-    return DT == F16 ? 4 * (r & 3) : 2 * (r & 7);
+    return DT == F16 ? 4 * (r & 3) : (DT == S8 ? 2 * (r & 7) : (r >> 1) & 7);
 }
 
 // Copy unit d of a stage for lane `lane`: A units as in the pipelined kernel;
@@ -63,7 +74,7 @@ __device__ __forceinline__ const uint8_t *tb_src(const uint8_t *A, const uint8_t
     const int u = d - P::A_UNITS;
     const int r = u * P::ROWS_PER_UNIT + lane / P::CHB;  // B row within the stage
     const int c = (lane % P::CHB) ^ tb_swz<DT>(r);
-    return B + (size_t)r * N * P::ES + (size_t)tn * P::RB + c * 16;
+    return B + (size_t)r * P::col_bytes(N) + (size_t)tn * P::RB + c * 16;
 }
 
 // One K-chunk's operand runs: A by ds_read_b128 (as load_runs), B by two
@@ -83,11 +94,11 @@ __device__ __forceinline__ void tb_load_runs(const uint8_t *st, int kc, int wm, 
 #pragma unroll
     for (int j = 0; j < T::FN; ++j) {
         const int col = wn * T::WTN + j * T::MS + 16 * (g & 1);  // first column of the group
-        const int byte = col * P::ES + (j16 % P::LPR) * 8;      // this lane's 8 bytes in the row
+        const int byte = (int)P::col_bytes(col) + (j16 % P::LPR) * 8;  // this lane's 8 bytes in the row
         i32x4 v;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            // k rows of this read: chunk kc's 16 (FP16) / 32 (INT8) k, half g / 2, part t
+            // k rows of this read: chunk kc's 16 (FP16) / 32 (INT8) / 64 (INT4) k, half g / 2, part t
             const int row = kc * (2 * 2 * P::RR) + (g >> 1) * (2 * P::RR) + t * P::RR + j16 / P::LPR;
             const uint8_t *p = sb + row * P::RB + ((((byte >> 4) ^ tb_swz<DT>(row))) << 4) + (byte & 15);
             typedef __attribute__((address_space(3))) void lds_void_t;
@@ -98,10 +109,16 @@ __device__ __forceinline__ void tb_load_runs(const uint8_t *st, int kc, int wm, 
                 const uint64_t u = __builtin_bit_cast(uint64_t, x);
                 v[2 * t] = (int)(uint32_t)u;
                 v[2 * t + 1] = (int)(uint32_t)(u >> 32);
-            } else {
+            } else if constexpr (DT == S8) {
                 typedef int v2i __attribute__((ext_vector_type(2)));
                 typedef __attribute__((address_space(3))) v2i lds_v2i;
                 const v2i x = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i *)(lds_void_t *)p);
+                v[2 * t] = x[0];
+                v[2 * t + 1] = x[1];
+            } else {
+                typedef int v2i __attribute__((ext_vector_type(2)));
+                typedef __attribute__((address_space(3))) v2i lds_v2i;
+                const v2i x = __builtin_amdgcn_ds_read_tr4_b64_v2i32((lds_v2i *)(lds_void_t *)p);
                 v[2 * t] = x[0];
                 v[2 * t + 1] = x[1];
             }
@@ -177,7 +194,7 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_tb(const uint8_t *_
     for (int j = 0; j < T::DMA_PER_WAVE; ++j)
         src[j] = tb_src<DT, T>(A, B, M, N, Kb, tm, tn, wave * T::DMA_PER_WAVE + j, lane);
     // per-slice advance: A waves by the slice's bytes, B waves by BK rows of B
-    const long stride = (wave * T::DMA_PER_WAVE < P::A_UNITS) ? (long)T::BKB : (long)P::BK * N * P::ES;
+    const long stride = (wave * T::DMA_PER_WAVE < P::A_UNITS) ? (long)T::BKB : (long)P::BK * P::col_bytes(N);
 
     acc_t acc[T::FM][T::FN];
 #pragma unroll
@@ -200,7 +217,10 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_tb(const uint8_t *_
 
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + (lane % 32);
-    epi_store_tile<DT, 32, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, lane / 32, M, N, ConvSame());
+    if constexpr (DT == S4)  // INT4 sums are carried times 256 (s4_lo_x16)
+        epi_store_tile<DT, 32, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, lane / 32, M, N, ConvShift8());
+    else
+        epi_store_tile<DT, 32, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, lane / 32, M, N, ConvSame());
 }
 
 }  // namespace mpg

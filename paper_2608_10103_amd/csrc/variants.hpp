@@ -163,11 +163,13 @@ Variant fp6(const char *name) {
 }
 
 // The one-wave-per-SIMD FP6 kernel (wide_f6.hpp); the table holds its
-// raw-sum instantiation, the launcher swaps in the other where needed.
-inline Variant fp6wide(const char *name) {
+// raw-sum instantiation, the launcher swaps in the other where needed. AUX:
+// cache policy of the copy loads.
+template <int AUX = CP_DEFAULT>
+Variant fp6wide(const char *name) {
     typedef void (*f6_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *,
                           int32_t *, int, int, int, int, int, int, int, EpiParams);
-    f6_fn f = &wide_f6_gemm<true>, fe = &wide_f6_gemm<false>;
+    f6_fn f = &wide_f6_gemm<true, AUX>, fe = &wide_f6_gemm<false, AUX>;
     return Variant{name, FP6WIDE, WideF6Cfg::BM, WideF6Cfg::BN, WideF6Cfg::J, WideF6Cfg::NTHREADS,
                    reinterpret_cast<const void *>(f), false, reinterpret_cast<const void *>(fe)};
 }
@@ -237,7 +239,7 @@ Variant generic(const char *name) {
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
 constexpr int kNumCommon = 54;
-constexpr int kNumFp6 = 13;
+constexpr int kNumFp6 = 16;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 
 // Kernel of the transposed-B entry point (tposeb.hip): F16 or S8, else null.

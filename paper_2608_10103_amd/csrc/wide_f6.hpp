@@ -65,14 +65,15 @@ struct WF6Copy {
     uint8_t *dp, *dq;                  // lds + run w's offset in a P / Q part
 };
 
-// copy load u (0..11) of slice ks into stage s
+// copy load u (0..11) of slice ks into stage s; AUX: cache policy
+template <int AUX>
 __device__ __forceinline__ void wf6_load(const WF6Copy &c, int u, int ks, int s) {
     typedef WideF6Cfg T;
     const int so = s * T::STAGE;
-    if (u < 4) wide_copy(c.ap, c.apn, c.dp + so + T::AP + u * 1024, c.voff, c.ap0 + ks * c.aps + u * 1024);
-    else if (u < 6) wide_copy(c.aq, c.aqn, c.dq + so + T::AQ + (u - 4) * 1024, c.voff, c.aq0 + ks * c.aqs + (u - 4) * 1024);
-    else if (u < 10) wide_copy(c.bp, c.bpn, c.dp + so + T::BP + (u - 6) * 1024, c.voff, c.bp0 + ks * c.bps + (u - 6) * 1024);
-    else wide_copy(c.bq, c.bqn, c.dq + so + T::BQ + (u - 10) * 1024, c.voff, c.bq0 + ks * c.bqs + (u - 10) * 1024);
+    if (u < 4) wide_copy<AUX>(c.ap, c.apn, c.dp + so + T::AP + u * 1024, c.voff, c.ap0 + ks * c.aps + u * 1024);
+    else if (u < 6) wide_copy<AUX>(c.aq, c.aqn, c.dq + so + T::AQ + (u - 4) * 1024, c.voff, c.aq0 + ks * c.aqs + (u - 4) * 1024);
+    else if (u < 10) wide_copy<AUX>(c.bp, c.bpn, c.dp + so + T::BP + (u - 6) * 1024, c.voff, c.bp0 + ks * c.bps + (u - 6) * 1024);
+    else wide_copy<AUX>(c.bq, c.bqn, c.dq + so + T::BQ + (u - 10) * 1024, c.voff, c.bq0 + ks * c.bqs + (u - 10) * 1024);
 }
 
 // One k-chunk: 16 MFMAs on (a, b); after MFMA 2 f, fragment f of the next
@@ -80,7 +81,7 @@ __device__ __forceinline__ void wf6_load(const WF6Copy &c, int u, int ks, int s)
 // first need them); after MFMA 2 u + 1, copy load U0 + u (u < 6) of slice ks
 // into stage s. pa/qa, pb/qb: LDS offsets of the P and Q parts of block 0
 // of the next set (f6_frag reads them).
-template <int U0>
+template <int U0, int AUX>
 __device__ __forceinline__ void wf6_chunk(const F6Frag (&a)[4], const F6Frag (&b)[4], f32x16 (&acc)[4][4],
                                           F6Frag (&na)[4], F6Frag (&nb)[4], const uint8_t *lds, int pa,
                                           int qa, int pb, int qb, const WF6Copy &c, int ks, int s) {
@@ -94,7 +95,7 @@ __device__ __forceinline__ void wf6_chunk(const F6Frag (&a)[4], const F6Frag (&b
             else if constexpr (f <= 4) nb[f - 1] = f6_frag(lds, pb + (f - 1) * 512, qb + (f - 1) * 256);
             else na[f - 4] = f6_frag(lds, pa + (f - 4) * 512, qa + (f - 4) * 256);
         } else if constexpr (m / 2 < 6) {
-            wf6_load(c, U0 + m / 2, ks, s);
+            wf6_load<AUX>(c, U0 + m / 2, ks, s);
         }
         __builtin_amdgcn_sched_barrier(0);
     });
@@ -103,8 +104,9 @@ __device__ __forceinline__ void wf6_chunk(const F6Frag (&a)[4], const F6Frag (&b
 // Ap/Aq, Bp/Bq: converted operands; Ma / Nb their padded row counts; KT =
 // padded K / 128 slices (at least 2: K is padded to 256). PLAIN: raw sums to
 // a row-major int32 C of whole 256 x 256 tiles, stored straight from the
-// accumulators; otherwise the shared epilogue (ragged edges, scales).
-template <bool PLAIN>
+// accumulators; otherwise the shared epilogue (ragged edges, scales). AUX:
+// cache policy of the copy loads.
+template <bool PLAIN, int AUX = CP_DEFAULT>
 __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
     const uint8_t *__restrict__ Ap, const uint8_t *__restrict__ Aq, const uint8_t *__restrict__ Bp,
     const uint8_t *__restrict__ Bq, int32_t *__restrict__ C, int M, int N, int Ma, int Nb, int KT,
@@ -161,11 +163,11 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
 
     // prologue: slices 0 and 1 whole, loads 0..5 of slice 2; wait for slice 0
 #pragma unroll
-    for (int u = 0; u < 12; ++u) wf6_load(c, u, 0, 0);
+    for (int u = 0; u < 12; ++u) wf6_load<AUX>(c, u, 0, 0);
 #pragma unroll
-    for (int u = 0; u < 12; ++u) wf6_load(c, u, 1, 1);
+    for (int u = 0; u < 12; ++u) wf6_load<AUX>(c, u, 1, 1);
 #pragma unroll
-    for (int u = 0; u < 6; ++u) wf6_load(c, u, min(2, KT - 1), 2);
+    for (int u = 0; u < 6; ++u) wf6_load<AUX>(c, u, min(2, KT - 1), 2);
     asm volatile("s_waitcnt vmcnt(18)\n\ts_barrier" ::: "memory");
     // chunk 0 of slice 0; then a wait the compiler knows of (lgkmcnt(0)),
     // so that at the loop head only the reads of the previous iteration are
@@ -181,10 +183,10 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
     for (int kt = 0; kt < KT; ++kt) {
         const int s0 = kt % 3, s1 = (kt + 1) % 3, s2 = (kt + 2) % 3;
         const int cur = s0 * T::STAGE, nxt = s1 * T::STAGE;
-        wf6_chunk<6>(ra[0], rb[0], acc, ra[1], rb[1], lds, pa0 + cur + KCP, qa0 + cur + KCQ, pb0 + cur + KCP,
+        wf6_chunk<6, AUX>(ra[0], rb[0], acc, ra[1], rb[1], lds, pa0 + cur + KCP, qa0 + cur + KCQ, pb0 + cur + KCP,
                      qb0 + cur + KCQ, c, min(kt + 2, KT - 1), s2);
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
-        wf6_chunk<0>(ra[1], rb[1], acc, ra[0], rb[0], lds, pa0 + nxt, qa0 + nxt, pb0 + nxt, qb0 + nxt, c,
+        wf6_chunk<0, AUX>(ra[1], rb[1], acc, ra[0], rb[0], lds, pa0 + nxt, qa0 + nxt, pb0 + nxt, qb0 + nxt, c,
                      min(kt + 3, KT - 1), s0);
     }
     // Clamped copies may still be landing. The last MFMA results: an XDL op

@@ -219,10 +219,12 @@ GEMM = {"f16": gemm_f16_f32, "s8": gemm_s8_s32, "s4": gemm_s4_s32}
 
 
 def gemm_bt(dtype: str, A, B_kn, C=None, stream=None):
-    """C = A * B with B given K x N row-major (N-contiguous), FP16 or INT8
-    (mpgemm_gemm_bt): A (M, K), B_kn (K, N) of the dtype's input type."""
-    if dtype not in ("f16", "s8"):
-        raise ValueError("transposed B: f16 or s8")
+    """C = A * B with B given K x N row-major (N-contiguous) (mpgemm_gemm_bt):
+    FP16 or INT8 A (M, K) and B_kn (K, N) of the dtype's input type, or INT4 A
+    (M, K/2) packed along K and B_kn (K, N/2) packed along N (uint8, low
+    nibble = even column)."""
+    if dtype not in ("f16", "s8", "s4"):
+        raise ValueError("transposed B: f16, s8 or s4")
     want = _IN_DTYPE[dtype]
     for name, t in (("A", A), ("B", B_kn)):
         if not isinstance(t, torch.Tensor) or t.dtype != want or t.dim() != 2:
@@ -233,6 +235,8 @@ def gemm_bt(dtype: str, A, B_kn, C=None, stream=None):
         raise ValueError("A and B must be on the same device")
     M, K = A.shape
     KB, N = B_kn.shape
+    if dtype == "s4":
+        K, N = 2 * K, 2 * N
     if K != KB:
         raise ValueError(f"K mismatch: A has {K}, B has {KB} rows")
     C = _out(dtype, M, N, A, C)

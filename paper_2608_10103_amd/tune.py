@@ -50,7 +50,7 @@ def main(argv=None) -> int:
     ap.add_argument("--vendor", action="store_true", help="also time the vendor library (FP16, INT8)")
     ap.add_argument("--transposed-b", action="store_true",
                     help="also time mpgemm_gemm_bt (B stored K x N row-major) on the same operands "
-                         "(FP16, INT8)")
+                         "(FP16, INT8, INT4)")
     args = ap.parse_args(argv)
     want = [w for w in args.variants.split(",") if w]
     stream = torch.cuda.Stream()
@@ -72,19 +72,27 @@ def main(argv=None) -> int:
                 if not mp.variant_supports(dt, v, M, N, K, Ad.data_ptr(), Bd.data_ptr()):
                     continue
                 if not split_list:
+                    # the automatic split of a call with a workspace (allocated here, once)
                     auto = mp.select_splits(dt, v, M, N, K)
                     runs.append((v, None, f"{name} (splits {auto})"))
                     continue
                 for sp in split_list:
-                    C = torch.empty((M, N), dtype=torch.float32 if dt == "f16" else torch.int32, device="cuda")
                     try:
-                        mp.GEMM[dt](Ad, Bd, C=C, variant=v, splits=sp)
+                        mp.workspace_size(dt, M, N, K, variant=v, splits=sp)
                     except mp.HipError:
                         continue
                     runs.append((v, sp, f"{name} splits {sp}"))
             Bt = None
-            if args.transposed_b and dt in ("f16", "s8"):
-                Bt = Bd.t().contiguous()  # the same B, K x N row-major
+            if args.transposed_b:
+                # the same B, K x N row-major (INT4: nibbles re-packed along N)
+                if dt == "s4":
+                    lo, hi = (B & 0xF).astype(np.int8), (B >> 4).astype(np.int8)
+                    logical = np.empty((N, K), np.int8)
+                    logical[:, 0::2] = np.where(lo >= 8, lo - 16, lo)
+                    logical[:, 1::2] = np.where(hi >= 8, hi - 16, hi)
+                    Bt = torch.from_numpy(si.pack_s4(np.ascontiguousarray(logical.T))).cuda()
+                else:
+                    Bt = Bd.t().contiguous()
                 runs.append(("bt", None, "transposed B (mpgemm_gemm_bt)"))
             if args.vendor and dt in ("f16", "s8"):
                 runs.append(("vendor", None, "vendor library (A x B^T)"))
@@ -95,6 +103,11 @@ def main(argv=None) -> int:
                               device="cuda") for r in runs]
             reps = max(2, min(200, int(2e11 / (2 * M * N * K))))
             times = [[] for _ in runs]
+            # each run's workspace (split K, FP6 pre-pass), zero-filled, allocated before timing
+            wss = []
+            for v, sp, _ in runs:
+                n = mp.workspace_size(dt, M, N, K, variant=v, splits=sp) if isinstance(v, int) else 0
+                wss.append(mp.new_workspace(n, "cuda") if n else None)
 
             def call(i):
                 v, sp, _ = runs[i]
@@ -106,7 +119,7 @@ def main(argv=None) -> int:
                     else:
                         torch._int_mm(Ad, Bd.t(), out=Cs[i])
                 else:
-                    mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp)
+                    mp.GEMM[dt](Ad, Bd, C=Cs[i], stream=stream, variant=v, splits=sp, workspace=wss[i])
 
             with torch.cuda.stream(stream):
                 for i in range(len(runs)):
@@ -128,7 +141,7 @@ def main(argv=None) -> int:
                 ms = float(np.median(times[i]))
                 tops = 2 * M * N * K / (ms * 1e-3) / 1e12
                 name = {"bt": "transposed_b", "vendor": "vendor"}.get(v) if isinstance(v, str) else mp.variant_name(dt, v)
-                peak = PEAK_FP6 if name.startswith("fp6") else PEAK[dt]
+                peak = PEAK_FP6 if name.startswith(("fp6", "e2m3")) else PEAK[dt]
                 if i == 0:
                     same = "ref"
                 elif dt == "f16":

@@ -738,46 +738,72 @@ def _gpu_gemm_bt(dtype, A, B_kn):
     return C.cpu().numpy()
 
 
-@pytest.mark.parametrize("dtype", ["f16", "s8"])
+def _to_kn(dtype, B):
+    """The oracle's B (N rows of K, INT4 packed along K) as the transposed-B
+    entry point takes it: K x N row-major (INT4 packed along N)."""
+    if dtype == "s4":
+        return si.pack_s4(np.ascontiguousarray(oracle.s4_unpack(B).T))
+    return np.ascontiguousarray(B.T)
+
+
+KSLICE = {"f16": 64, "s8": 128, "s4": 256}
+
+
+@pytest.mark.parametrize("dtype", ["f16", "s8", "s4"])
 def test_transposed_b_parity(dtype):
-    """mpgemm_gemm_bt (B(k, j) at k * N + j) against the oracle on the same
-    B transposed on the host to the oracle's N rows of K: several tiles and
-    K-slices, the 2-slice ring's steady state and tail, ragged M."""
-    kslice = 64 if dtype == "f16" else 128
+    """mpgemm_gemm_bt (B(k, j) at k * N + j; INT4 packed along N) against the
+    oracle on the same B transposed on the host to the oracle's N rows of K:
+    several tiles and K-slices, the 2-slice ring's steady state and tail,
+    ragged M."""
+    kslice = KSLICE[dtype]
     for (M, N, K) in [(256, 256, kslice), (512, 768, 5 * kslice), (300, 256, 3 * kslice),
                       (1, 512, 2 * kslice), (777, 1024, 7 * kslice)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=900 + M + N + K)  # B: N rows of K
-        B_kn = np.ascontiguousarray(B.T)  # the same matrix, K x N row-major
-        C = _gpu_gemm_bt(dtype, A, B_kn)
+        C = _gpu_gemm_bt(dtype, A, _to_kn(dtype, B))
         assert_parity(dtype, C, *oracle_gemm(dtype, A, B), f"{dtype} transposed B {M}x{N}x{K}")
     _log(f"{dtype} transposed B: ok")
 
 
-@pytest.mark.parametrize("dtype", ["f16", "s8"])
+@pytest.mark.parametrize("dtype", ["f16", "s8", "s4"])
 def test_transposed_b_full_size_sampled_rows(dtype):
     """N = 8192 (the measured size): 40 sampled rows against the oracle."""
     n = 8192
     A, B = si.gen_operands(dtype, n, n, n, seed=31)
-    C = _gpu_gemm_bt(dtype, A, np.ascontiguousarray(B.T))
+    C = _gpu_gemm_bt(dtype, A, _to_kn(dtype, B))
     rows = np.random.default_rng(31).choice(n, size=38, replace=False).tolist() + [0, n - 1]
     C_ref, D = oracle_gemm(dtype, A, B, rows=rows)
     assert_parity(dtype, C[rows], C_ref, D, f"{dtype} transposed B {n}^3 sampled rows")
 
 
 def test_transposed_b_closed_forms():
-    """Identity as B: C = A exactly (integer-valued FP16, INT8); all-ones:
-    C = K."""
-    for dtype, K in (("f16", 256), ("s8", 256)):
+    """Identity as B: C = A exactly (integer-valued FP16, INT8, INT4); all-ones:
+    C = K; INT4: every nibble value in every position of B's packed rows."""
+    for dtype, K in (("f16", 256), ("s8", 256), ("s4", 512)):
         M = N = 256
-        vals = np.random.default_rng(5).integers(-8, 9, size=(M, K))
-        A = vals.astype(np.float16) if dtype == "f16" else vals.astype(np.int8)
-        eye = np.eye(K, N, dtype=A.dtype)
+        vals = np.random.default_rng(5).integers(-8, 8, size=(M, K))
+        if dtype == "s4":
+            A = si.pack_s4(vals.astype(np.int8))
+            eye = si.pack_s4(np.eye(K, N, dtype=np.int8))
+            ones_a = np.full((M, K // 2), 0x11, np.uint8)
+            ones_b = np.full((K, N // 2), 0x11, np.uint8)
+        else:
+            A = vals.astype(np.float16) if dtype == "f16" else vals.astype(np.int8)
+            eye = np.eye(K, N, dtype=A.dtype)
+            ones_a, ones_b = np.ones((M, K), dtype=A.dtype), np.ones((K, N), dtype=A.dtype)
         C = _gpu_gemm_bt(dtype, A, eye)
-        want = A[:, :N].astype(np.float32) if dtype == "f16" else A[:, :N].astype(np.int32)
+        want = vals[:, :N].astype(np.float32 if dtype == "f16" else np.int32)
         assert np.array_equal(C, want), dtype
-        ones_a = np.ones((M, K), dtype=A.dtype)
-        ones_b = np.ones((K, N), dtype=A.dtype)
         assert np.all(_gpu_gemm_bt(dtype, ones_a, ones_b) == K), dtype
+    # INT4: A = I (K = 512) and B cycling through all 256 byte values along N:
+    # C = B logically, so every nibble of both halves of a byte is decoded
+    K, N = 512, 512
+    Bkn = (np.arange(K * (N // 2)) % 256).astype(np.uint8).reshape(K, N // 2)
+    lo, hi = (Bkn & 0xF).astype(np.int64), (Bkn >> 4).astype(np.int64)
+    want = np.empty((K, N), np.int64)
+    want[:, 0::2] = np.where(lo >= 8, lo - 16, lo)
+    want[:, 1::2] = np.where(hi >= 8, hi - 16, hi)
+    C = _gpu_gemm_bt("s4", si.pack_s4(np.eye(K, dtype=np.int8)), Bkn)
+    assert np.array_equal(C.astype(np.int64), want)
 
 
 def test_transposed_b_argument_errors():
@@ -788,9 +814,14 @@ def test_transposed_b_argument_errors():
         with pytest.raises(mp.HipError):
             bad()
     with pytest.raises(ValueError):
-        mp.gemm_bt("s4", Ad, Bd)
+        mp.gemm_bt("bf16", Ad, Bd)
+    a4 = torch.zeros((256, 64), dtype=torch.uint8, device="cuda")    # INT4 K = 128: off the 256-k slice
+    b4 = torch.zeros((128, 128), dtype=torch.uint8, device="cuda")
+    with pytest.raises(mp.HipError):
+        mp.gemm_bt("s4", a4, b4)
     L = mp.lib()
-    assert L.mpgemm_gemm_bt(2, 256, 256, 64, Ad.data_ptr(), Bd.data_ptr(), Ad.data_ptr(), None) != 0
+    assert L.mpgemm_gemm_bt(3, 256, 256, 64, Ad.data_ptr(), Bd.data_ptr(), Ad.data_ptr(), None) != 0
+    assert L.mpgemm_gemm_bt(2, 256, 256, 256, Ad.data_ptr(), Bd.data_ptr(), Ad.data_ptr(), None) != 0  # C on A
     assert L.mpgemm_gemm_bt(0, 256, 256, 64, Ad.data_ptr() + 2, Bd.data_ptr(), None, None) != 0
     # K = 0: zero fill
     C = torch.full((4, 256), 7.0, dtype=torch.float32, device="cuda")
