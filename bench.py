@@ -129,10 +129,18 @@ def main():
                          "the same of a --copy-mib run) -> profiles/traffic.json")
     ap.add_argument("--copy-mib-ref", type=int, default=256,
                     help="size of the copy the calibration folders were taken on")
+    ap.add_argument("--counters-table", nargs="+", metavar="KIND=FOLDER",
+                    help="print a per-point counter table from rocprofv3 --pmc folders of this "
+                         "script's runs over --points: mfma= (SQ_VALU_MFMA_BUSY_CYCLES, SQ_WAVES, "
+                         "SQ_WAVE_CYCLES, SQ_LDS_BANK_CONFLICT, GRBM_GUI_ACTIVE), fetch= (FETCH_SIZE), "
+                         "write= (WRITE_SIZE), copyfetch= and copywrite= (the same of a --copy-mib run)")
     args = ap.parse_args()
 
     if args.ingest_pmc:
         ingest_pmc(args)
+        return
+    if args.counters_table:
+        counters_table(args)
         return
 
     if args.gpus != 1:
@@ -387,6 +395,110 @@ def ingest_pmc(args):
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
     print(json.dumps(out))
+
+
+def _dispatches(folder):
+    """Library dispatches of a rocprofv3 --pmc CSV folder in dispatch order:
+    [(kernel name, {counter: value}, duration in ns)]."""
+    import csv
+    import glob
+    rows = {}
+    for f in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if "mpg::" not in r["Kernel_Name"]:
+                continue
+            d = rows.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"], {},
+                                                         int(r["End_Timestamp"]) - int(r["Start_Timestamp"])])
+            d[1][r["Counter_Name"]] = float(r["Counter_Value"])
+    if not rows:
+        raise SystemExit(f"no library dispatches in {folder}")
+    return [tuple(rows[k]) for k in sorted(rows)]
+
+
+def counters_table(args):
+    """Per-point counters of runs of this script over --points (every step
+    launches the same library kernels in the same order: the INT4 FP6 pre-pass,
+    where the chosen kernel needs one, then the GEMM). Medians over the runs'
+    steps. Clock = GRBM_GUI_ACTIVE / 8 XCDs / duration; MFMA busy =
+    SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x cycles); waves per SIMD =
+    4 SQ_WAVE_CYCLES (counted in 4-cycle units) / (1024 x cycles); LDS bank
+    conflicts per CU-cycle = SQ_LDS_BANK_CONFLICT / (256 x cycles); HBM-side
+    bytes = FETCH_SIZE / read scale + WRITE_SIZE / write scale, the scales
+    being what the same counters read per byte of a plain copy."""
+    import paper_2608_10103_amd as mp
+    folders = dict(kv.split("=", 1) for kv in args.counters_table)
+    pts = parse_points(args.points)
+    seq = []  # (point index, kernel role) per dispatch of one step
+    for i, (dt, n, _) in enumerate(pts):
+        name = mp.variant_name(dt, mp.select_variant(dt, n, n, n, with_ws=dt in WS_DTYPES))
+        if name.startswith("fp6"):
+            seq.append((i, "pre-pass"))
+        seq.append((i, name))
+    per = {}
+    for kind, folder in folders.items():
+        if kind.startswith("copy"):
+            continue
+        ds = _dispatches(folder)
+        if len(ds) % len(seq):
+            raise SystemExit(f"{folder}: {len(ds)} dispatches, not a multiple of {len(seq)} per step")
+        for j, (kname, cnt, dur) in enumerate(ds):
+            slot = per.setdefault(j % len(seq), {"kernel": kname, "dur": [], "c": {}})
+            if kind == "mfma":
+                slot["dur"].append(dur)
+            for c, v in cnt.items():
+                slot["c"].setdefault(c if c != "GRBM_GUI_ACTIVE" else f"GRBM_{kind}", []).append((v, dur))
+    scale = {}
+    for kind, cname in (("copyfetch", "FETCH_SIZE"), ("copywrite", "WRITE_SIZE")):
+        if kind in folders:
+            vals = [c[cname] for _, c, _ in _dispatches_any(folders[kind]) if cname in c]
+            scale[cname] = float(np.median(vals)) / (args.copy_mib_ref * 1024.0)
+    med = lambda xs: float(np.median(xs)) if xs else float("nan")
+    print("| point | kernel | median us | clock GHz | MFMA busy | waves/SIMD | LDS conflicts per CU-cycle | "
+          "FETCH KiB | WRITE KiB | HBM-side MB | HBM GB/s | algorithmic MB | traffic / algorithmic |")
+    print("|---|---|---|---|---|---|---|---|---|---|---|---|---|")
+    for j, (i, role) in enumerate(seq):
+        dt, n, _ = pts[i]
+        slot = per.get(j)
+        if slot is None:
+            continue
+        c = slot["c"]
+        dur_ns = med(slot["dur"]) if slot["dur"] else med([d for _, d in c.get("GRBM_fetch", [])])
+        cyc = med([v for v, _ in c.get("GRBM_mfma", [])]) / 8.0
+
+        def per_cycle(name, denom):
+            xs = [v for v, _ in c.get(name, [])]
+            return med(xs) / (denom * cyc) if xs and cyc > 0 else float("nan")
+        clock = cyc / dur_ns if dur_ns > 0 else float("nan")
+        mfma = per_cycle("SQ_VALU_MFMA_BUSY_CYCLES", 1024.0)
+        waves = 4.0 * per_cycle("SQ_WAVE_CYCLES", 1024.0)
+        lds = per_cycle("SQ_LDS_BANK_CONFLICT", 256.0)
+        fk = med([v for v, _ in c.get("FETCH_SIZE", [])])
+        wk = med([v for v, _ in c.get("WRITE_SIZE", [])])
+        hbm = (fk / scale["FETCH_SIZE"] + wk / scale["WRITE_SIZE"]) * 1024.0 if scale and fk == fk and wk == wk \
+            else float("nan")
+        # bytes per operand element the kernel reads: the FP6 GEMM reads the
+        # pre-pass's 6-bit codes
+        elem = 0.75 if role.startswith("fp6") else {"f16": 2.0, "s8": 1.0, "s4": 0.5}[dt]
+        alg = 2 * n * n * elem + 4.0 * n * n if role != "pre-pass" else 2 * n * n * 0.5 + 2 * n * n * 0.75
+        kname = slot["kernel"].split("(")[0].replace("void ", "")
+        label = f"{dt} {n}" + (" (pre-pass)" if role == "pre-pass" else "")
+        print(f"| {label} | `{kname}` | {dur_ns / 1e3:.1f} | {clock:.2f} | {100 * mfma:.1f}% | {waves:.2f} | "
+              f"{lds:.4f} | {fk:.0f} | {wk:.0f} | {hbm / 1e6:.1f} | {hbm / dur_ns:.0f} | {alg / 1e6:.1f} | "
+              f"{hbm / alg:.2f} |")
+
+
+def _dispatches_any(folder):
+    """Every dispatch of a folder (the copy runs launch torch's kernels)."""
+    import csv
+    import glob
+    rows = {}
+    for f in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            if "copy" not in r["Kernel_Name"].lower():
+                continue
+            d = rows.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"], {}, 0])
+            d[1][r["Counter_Name"]] = float(r["Counter_Value"])
+    return [tuple(rows[k]) for k in sorted(rows)]
 
 
 def cpu_baseline(bufs, log):

@@ -254,6 +254,35 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
  * or size. */
 int mpgemm_select_splits(int dtype, int variant, int M, int N, int K);
 
+/* Stream-K: the variants named "..._sk" (the one-wave-per-SIMD FP16/INT8
+ * kernel, the 256x256 and the 128x128 pipelined kernels) share the last,
+ * partly filled round of a problem's tiles out over more workgroups. With T
+ * tiles, G workgroups resident at once (one per CU: 256 on MI355X) and
+ * T = q G + r, 0 < r <= G / 2: workgroups 0 .. q G - 1 compute one whole tile
+ * each; the K-slices (KT per tile, 128 bytes of K each) of each of the r
+ * remaining tiles are then cut into s contiguous parts, one workgroup each,
+ * s = round(sqrt(KT / 5)) capped at G / r and 8. The last of a tile's parts
+ * to finish adds the s partial tiles in part order and writes C, so results
+ * do not depend on scheduling (FP16: the order of summation differs from
+ * the whole-tile kernel's, within the same error bound; integers: exact).
+ * Scratch, in the workspace: the 64 KiB counter block (one counter per
+ * tile, left zero by every call), then r * s partial tiles of 4 x BM x BN
+ * bytes. Every tile is computed whole (no scratch) without a large enough
+ * workspace, when T is a multiple of G, r > G / 2, T is beyond 16384 tiles,
+ * s < 2, or the expected gain, KT (1 - 1/s) - 5 (s - 1) - 13 slice-times,
+ * is at most KT / 10. With a workspace the automatic choice takes a
+ * stream-K variant in place of its whole-tile kernel where its schedule is
+ * on.
+ * mpgemm_sk_schedule: the schedule a stream-K variant would use for this
+ * problem on the current device (G = 256 when no device is visible):
+ * *dp_tiles whole tiles first, then *parts parts per remaining tile (1:
+ * stream-K off), *grid workgroups in all. hipErrorInvalidValue for an
+ * invalid dtype or variant, null outputs, or a problem the variant cannot
+ * run; for a variant without a stream-K schedule it reports every tile
+ * whole. Host only: enqueues nothing. */
+hipError_t mpgemm_sk_schedule(int dtype, int variant, int M, int N, int K, int *dp_tiles, int *parts,
+                              int *grid);
+
 /* One specific variant with an explicit split count (0 = the automatic
  * choice for the variant), scaled outputs when epi is not NULL, and a
  * workspace as for mpgemm_gemm_ws. hipErrorInvalidValue also when the

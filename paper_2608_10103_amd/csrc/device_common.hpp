@@ -276,21 +276,32 @@ __global__ __launch_bounds__(256) void row_sums(const uint8_t *__restrict__ X, i
     if (threadIdx.x == 0) out[blockIdx.x] = part[0] + part[1] + part[2] + part[3];
 }
 
-// Workgroup id -> (tile row, tile column). Workgroups are dispatched
-// round-robin over the 8 XCDs, each with its own L2; ids are first regrouped
-// so each XCD owns a contiguous run of the ordering, and the ordering walks
-// group_m tile rows at a time so concurrently running tiles share A row
-// panels and B column panels.
-__device__ __forceinline__ void tile_coords(int pid, int ntiles, int tiles_m, int tiles_n,
-                                            int group_m, int &tm, int &tn) {
-    if ((ntiles & 7) == 0) pid = (pid & 7) * (ntiles >> 3) + (pid >> 3);
+// Rank of workgroup `id` of `n` in an order where each XCD owns a
+// contiguous run: workgroups are dispatched round-robin over the 8 XCDs,
+// each with its own L2, so ids id, id + 8, ... share one. The identity when
+// n is not a multiple of 8.
+__device__ __forceinline__ int xcd_rank(int id, int n) {
+    return (n & 7) ? id : (id & 7) * (n >> 3) + (id >> 3);
+}
+
+// Linear tile index -> (tile row, tile column), walking group_m tile rows
+// at a time so that consecutive indices share A row panels and B column
+// panels.
+__device__ __forceinline__ void grouped_tile(int t, int tiles_m, int tiles_n, int group_m, int &tm, int &tn) {
     const int width = group_m * tiles_n;
-    const int group = pid / width;
+    const int group = t / width;
     const int first_m = group * group_m;
     const int gsize = min(tiles_m - first_m, group_m);
-    const int in_group = pid - group * width;
+    const int in_group = t - group * width;
     tm = first_m + in_group % gsize;
     tn = in_group / gsize;
+}
+
+// Workgroup id -> (tile row, tile column): XCD-contiguous ranks in grouped
+// order, so the workgroups that run together on one XCD share panels.
+__device__ __forceinline__ void tile_coords(int pid, int ntiles, int tiles_m, int tiles_n,
+                                            int group_m, int &tm, int &tn) {
+    grouped_tile(xcd_rank(pid, ntiles), tiles_m, tiles_n, group_m, tm, tn);
 }
 
 }  // namespace mpg

@@ -9,8 +9,10 @@
 // zero-point row sums) take it from a workspace the caller passes in.
 #include <hip/hip_runtime.h>
 #include <limits.h>
+#include <math.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <mutex>
 
 #include "mpgemm.h"
@@ -82,6 +84,8 @@ constexpr long kF6MaxRows = 65535L * 32;
 constexpr int kSplitCounters = 16384;
 constexpr size_t kSplitCounterBytes = (size_t)kSplitCounters * 4;
 
+constexpr int kMaxDevices = 64;
+
 bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, const void *B,
               const void *C) {
     if (v.kind == GENERIC) return true;
@@ -96,7 +100,7 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
         if (dtype == S4 && K >= 131072) return false;  // INT4 sums carried times 256
         return true;
     }
-    if (v.kind == WIDE) {
+    if (v.kind == WIDE || v.kind == WIDE_SK) {
         // whole 256 x 256 tiles and 128-byte K-slices, 16-byte aligned rows;
         // the copy buffers span 128 rows of K bytes (32-bit range)
         if (!v.fn || M % v.bm || N % v.bn) return false;
@@ -146,6 +150,65 @@ bool splits_ok(int dtype, const Variant &v, int M, int N, int K, int splits) {
     return row_bytes(dtype, K) % ((long)v.bkb * splits) == 0;
 }
 
+// Workgroups of the stream-K kernels resident at once on the current device:
+// one per CU (their LDS use allows no second). 256, MI355X's count, when no
+// device is visible (size queries on a host without one).
+int resident_groups() {
+    static std::atomic<int> cus[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (n > 0) return n;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
+// Stream-K schedule of a call (stream_k.hpp): with T tiles, G resident
+// workgroups and T = q G + r, 0 < r <= G / 2, the first q G tiles whole,
+// then the r remaining tiles in `parts` K-parts each. Off (every tile whole,
+// one workgroup each) for other variants, when the tiles fill whole rounds
+// or the last round more than half, beyond the counter block, or where the
+// cost model below expects no gain.
+//
+// Cost model, in units of one K-slice of one tile (about 1 us for a 256 x
+// 256 tile on MI355X, FP16 and INT8 alike, and proportionally less for
+// 128 x 128 tiles, whose partials are proportionally smaller): a tile's
+// last-round time without stream-K is KT slices; with s parts it is KT / s,
+// plus about 5 per partial tile the finishing part loads (s - 1; one
+// workgroup reads them at about 50 GB/s) and about 13 for publishing,
+// fencing and counting (timelines of the kernels at 4352 x 4096 x
+// {4096, 8192}). Gain(s) = KT (1 - 1/s) - 5 (s - 1) - 13 peaks near
+// s = sqrt(KT / 5); stream-K is taken when that gain exceeds a tenth of KT
+// (K-ranges of about 48 slices and more: FP16 K >= 3072, INT8 K >= 6144 with
+// 256 x 256 tiles).
+struct SkPlan {
+    bool on;
+    int dp_tiles, parts, grid;
+};
+
+constexpr int kSkMaxParts = 8;
+
+bool is_sk(const Variant &v) { return v.kind == TILED_SK || v.kind == WIDE_SK; }
+
+SkPlan sk_off(long tiles) { return SkPlan{false, (int)tiles, 1, (int)tiles}; }
+
+SkPlan sk_plan(int dtype, const Variant &v, int M, int N, int K) {
+    const long tiles = tile_count(v, M, N);
+    if (!is_sk(v) || tiles > kSplitCounters) return sk_off(tiles);
+    const long G = resident_groups(), r = tiles % G;
+    if (r == 0 || 2 * r > G) return sk_off(tiles);
+    const long KT = row_bytes(dtype, K) / v.bkb;
+    long parts = (long)(sqrt((double)KT / 5.0) + 0.5);
+    if (parts > G / r) parts = G / r;
+    if (parts > kSkMaxParts) parts = kSkMaxParts;
+    if (parts < 2) return sk_off(tiles);
+    const double gain = KT * (1.0 - 1.0 / parts) - 5.0 * (parts - 1) - 13.0;
+    if (gain <= 0.1 * KT) return sk_off(tiles);
+    const long dp = tiles - r;
+    return SkPlan{true, (int)dp, (int)parts, (int)(dp + r * parts)};
+}
+
 // Narrow-tile variants (select_narrow): three tiles with the small side on
 // A's rows, then the same three mirrored.
 constexpr int V_NARROW = 44;  // spread32x64_w1x2_k128_s4_m16, 32x128, 64x128; 64x32, 128x32, 128x64
@@ -192,6 +255,16 @@ enum : int {
     V_SKINNY = 38,           // skinny16x16_k64; then 16x32, 32x16, 32x32
     V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
 };
+// The stream-K schedules of three of them, the last entries of the common
+// list.
+constexpr int V_WIDE_SK = kNumCommon - 3, V_PIPE256_SK = kNumCommon - 2, V_SPREAD128_SK = kNumCommon - 1;
+
+int sk_twin(int variant) {
+    return variant == V_WIDE ? V_WIDE_SK
+                             : (variant == V_PIPE256_W2X4 ? V_PIPE256_SK
+                                                          : (variant == V_SPREAD128_K128 ? V_SPREAD128_SK : -1));
+}
+
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumCommon + 1;  // fp6pipe256x256_w2x4_k128_s2
 constexpr int V_FP6_WIDE = kNumCommon + 8;    // fp6wide256x256_w2x2_k128_s3
@@ -330,7 +403,15 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
         // skip a tile that would mostly compute padding
         if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < n) continue;
-        if (tm * tn * choose_splits(dtype, v, M, N, K) >= prefs[i].min_tiles) return prefs[i].variant;
+        if (tm * tn * choose_splits(dtype, v, M, N, K) >= prefs[i].min_tiles) {
+            // with a workspace, the stream-K schedule of the same kernel where
+            // its plan is on
+            const int twin = sk_twin(prefs[i].variant);
+            if (with_ws && twin >= 0 && supports(dtype, t[twin], M, N, K, A, B, C) &&
+                sk_plan(dtype, t[twin], M, N, K).on)
+                return twin;
+            return prefs[i].variant;
+        }
     }
     return 0;
 }
@@ -348,10 +429,11 @@ struct WsPlan {
     size_t sums_off, data_off, total;  // total 0: no workspace needed
 };
 
-WsPlan ws_plan(const Variant &v, int splits, int M, int N, int K, bool zero_points) {
+WsPlan ws_plan(const Variant &v, int splits, int M, int N, int K, bool zero_points, const SkPlan &sk) {
     const size_t sums = zero_points ? align_up(((size_t)M + N) * 4) : 0;
     size_t data = 0;
     if (splits > 1) data = (size_t)tile_count(v, M, N) * splits * v.bm * v.bn * 4;
+    else if (sk.on) data = (size_t)(sk.grid - sk.dp_tiles) * v.bm * v.bn * 4;  // one slot per split part
     else if (v.kind == FP6 || v.kind == FP6WIDE) data = F6Geom::bytes(M, K) + F6Geom::bytes(N, K);
     if (!sums && !data) return WsPlan{0, 0, 0};
     return WsPlan{kSplitCounterBytes, kSplitCounterBytes + sums, kSplitCounterBytes + sums + data};
@@ -392,7 +474,7 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
     return e;
 }
 
-hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, const void *A,
+hipError_t launch(int dtype, const Variant &v, int splits, const SkPlan &sk, int M, int N, int K, const void *A,
                   const void *B, void *C, EpiParams epi, const WsPlan &plan, Ws ws, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
@@ -413,6 +495,16 @@ hipError_t launch(int dtype, const Variant &v, int splits, int M, int N, int K, 
     }
     int kb = (int)row_bytes(dtype, K);
     int tiles_m = (M + v.bm - 1) / v.bm, tiles_n = (N + v.bn - 1) / v.bn;
+    if (is_sk(v)) {
+        SkArgs sa{sk.dp_tiles, sk.parts, nullptr, nullptr};
+        if (sk.on) {
+            sa.counters = reinterpret_cast<int *>(ws.p);
+            sa.partials = reinterpret_cast<uint32_t *>(ws.p + plan.data_off);
+        }
+        const void *fn = (v.kind == WIDE_SK && epi.out != OUT_PLAIN) ? v.fn_epi : v.fn;
+        void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &sa, &epi};
+        return hipLaunchKernel(fn, dim3(sk.grid), dim3(v.threads), args, 0, stream);
+    }
     if (!v.splitk) {
         const void *fn = v.fn;
         // the one-wave-per-SIMD kernels' table entries store raw sums of whole
@@ -480,6 +572,7 @@ bool valid_epilogue(int dtype, const mpgemm_epilogue *e) {
 // holds the split's scratch), validated; the workspace plan of that choice.
 struct Choice {
     int variant, splits;
+    SkPlan sk;
     WsPlan plan;
 };
 
@@ -491,17 +584,22 @@ hipError_t choose(int dtype, int variant, int splits, int M, int N, int K, const
         // (the FP6 pre-pass operands; split K is decided below), else the
         // choice without one
         variant = select_variant(dtype, M, N, K, A, B, C, ws_bytes > 0);
-        if (ws_plan(t[variant], 1, M, N, K, zero_points).total > ws_bytes)
+        const Variant &v = t[variant];
+        if (ws_plan(v, 1, M, N, K, zero_points, sk_plan(dtype, v, M, N, K)).total > ws_bytes)
             variant = select_variant(dtype, M, N, K, A, B, C, false);
     }
     if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
-    if (!supports(dtype, t[variant], M, N, K, A, B, C)) return hipErrorInvalidValue;
+    const Variant &v = t[variant];
+    if (!supports(dtype, v, M, N, K, A, B, C)) return hipErrorInvalidValue;
     if (splits < 0) {
-        splits = choose_splits(dtype, t[variant], M, N, K);
-        if (splits > 1 && ws_plan(t[variant], splits, M, N, K, zero_points).total > ws_bytes) splits = 1;
+        splits = choose_splits(dtype, v, M, N, K);
+        if (splits > 1 && ws_plan(v, splits, M, N, K, zero_points, SkPlan{}).total > ws_bytes) splits = 1;
     }
-    if (!splits_ok(dtype, t[variant], M, N, K, splits)) return hipErrorInvalidValue;
-    out = Choice{variant, splits, ws_plan(t[variant], splits, M, N, K, zero_points)};
+    if (!splits_ok(dtype, v, M, N, K, splits)) return hipErrorInvalidValue;
+    // a stream-K variant without room for its partial tiles runs every tile whole
+    SkPlan sk = sk_plan(dtype, v, M, N, K);
+    if (sk.on && ws_plan(v, splits, M, N, K, zero_points, sk).total > ws_bytes) sk = sk_off(tile_count(v, M, N));
+    out = Choice{variant, splits, sk, ws_plan(v, splits, M, N, K, zero_points, sk)};
     return hipSuccess;
 }
 
@@ -540,7 +638,7 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
         e = zero_point_sums(dtype, M, N, K, A, B, epi, reinterpret_cast<int *>(ws.p + ch.plan.sums_off), stream);
         if (e != hipSuccess) return e;
     }
-    return launch(dtype, table(dtype)[ch.variant], ch.splits, M, N, K, A, B, C, epi, ch.plan, ws, stream);
+    return launch(dtype, table(dtype)[ch.variant], ch.splits, ch.sk, M, N, K, A, B, C, epi, ch.plan, ws, stream);
 }
 
 // ---- scratch for callers that cannot allocate (mpgemm_gemm_noalloc) ----
@@ -551,8 +649,6 @@ hipError_t run(int dtype, int variant, int splits, int M, int N, int K, const vo
 constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
 static_assert(kStaticScratchBytes % kWsAlign == 0, "whole workspace granules");
 __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
-
-constexpr int kMaxDevices = 64;
 
 hipError_t static_scratch(uint8_t **out) {
     static std::mutex mu;
@@ -678,7 +774,7 @@ hipError_t mpgemm_gemm_noalloc(int dtype, int M, int N, int K, const void *A, co
         e = static_scratch(&ws);
         if (e != hipSuccess) return e;
     }
-    if (ch.splits > 1) {
+    if (ch.splits > 1 || ch.sk.on) {
         // the array keeps the last call's contents: clear the tile counters
         uint32_t *words = reinterpret_cast<uint32_t *>(ws);
         int n = (int)tile_count(table(dtype)[ch.variant], M, N);
@@ -731,6 +827,21 @@ hipError_t mpgemm_run_variant_ws(int dtype, int variant, int splits, int M, int 
     if (variant < 0 || splits < 0) return hipErrorInvalidValue;
     return run(dtype, variant, splits == 0 ? -1 : splits, M, N, K, A, B, C, stream, epi,
                Ws{static_cast<uint8_t *>(workspace), workspace_bytes});
+}
+
+hipError_t mpgemm_sk_schedule(int dtype, int variant, int M, int N, int K, int *dp_tiles, int *parts,
+                              int *grid) {
+    const Variant *t = table(dtype);
+    if (!t || variant < 0 || variant >= num_variants(dtype) || !dp_tiles || !parts || !grid)
+        return hipErrorInvalidValue;
+    if (M <= 0 || N <= 0 || K <= 0 || (dtype == S4 && (K & 1)) ||
+        !supports(dtype, t[variant], M, N, K, nullptr, nullptr, nullptr))
+        return hipErrorInvalidValue;
+    const SkPlan sk = sk_plan(dtype, t[variant], M, N, K);
+    *dp_tiles = sk.dp_tiles;
+    *parts = sk.parts;
+    *grid = sk.grid;
+    return hipSuccess;
 }
 
 int mpgemm_select_splits(int dtype, int variant, int M, int N, int K) {

@@ -404,32 +404,27 @@ __device__ __forceinline__ bool splitk_fixup(typename Acc<DT, T::MS>::type (&acc
 // which workgroup finishes last), writes C and resets the counter to zero for
 // the next call. No workgroup waits for another. The counters must be zero
 // before the first call.
+// Accumulate K-slices [kt0, kt0 + KT) of tile (tm, tn) into acc (zeroed
+// here) with the pipelined schedule above. On return every copy has landed;
+// the waves may still be reading LDS, so a caller that reuses the buffers
+// for another tile needs a barrier first.
 template <int DT, class T, bool SPREAD>
-__global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *__restrict__ A,
-                                                               const uint8_t *__restrict__ B,
-                                                               void *__restrict__ Cv, int M,
-                                                               int N, int Kb, int tiles_m,
-                                                               int tiles_n, int splits,
-                                                               int *__restrict__ counters,
-                                                               uint32_t *__restrict__ partials,
-                                                               EpiParams epi) {
-    static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
+__device__ __forceinline__ void pf_accumulate(uint8_t *lds, const uint8_t *A, const uint8_t *B, int M,
+                                              int N, int Kb, int tm, int tn, int kt0, int KT,
+                                              typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN]) {
     typedef typename Acc<DT, T::MS>::type acc_t;
     constexpr int S = T::STAGES;
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
-
-    const int tid = threadIdx.x;
+    // the lane's addresses derive from an opaque copy of the thread id, so a
+    // caller that accumulates several tiles in a loop recomputes them per
+    // tile instead of keeping them live through its epilogues
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane % T::MS, h = lane / T::MS;
     const int wm = wave / T::WGN, wn = wave % T::WGN;
-    const int ntiles = tiles_m * tiles_n;
-    const int split = blockIdx.x / ntiles, pid = blockIdx.x - split * ntiles;
-    int tm, tn;
-    tile_coords(pid, ntiles, tiles_m, tiles_n, T::GROUP_M, tm, tn);
-    const int kb_len = Kb / splits;  // K bytes of this workgroup; a multiple of BKB
-    A += (size_t)split * kb_len;
-    B += (size_t)split * kb_len;
+    A += (size_t)kt0 * T::BKB;
+    B += (size_t)kt0 * T::BKB;
 
     const uint8_t *src[T::DMA_PER_WAVE];
 #pragma unroll
@@ -438,13 +433,11 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
         src[j] = stage_src<T>(A, B, M, N, Kb, tm, tn, d, lane);
     }
 
-    acc_t acc[T::FM][T::FN];
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
         for (int j = 0; j < T::FN; ++j) acc[i][j] = acc_t{};
 
-    const int KT = kb_len / T::BKB;
     // Fill the ring (all S buffers; S - 1 when later copies are spread over
     // the slices), then wait for slice 0.
     constexpr int PRE = SPREAD ? S - 1 : S;
@@ -464,16 +457,60 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *_
         pf_slice<DT, T, true, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
     for (; kt < KT; ++kt)
         pf_slice<DT, T, false, SPREAD>(lds, src, wave, kt, wm, wn, r, h, ra, rb, acc);
+}
 
-    if (splits > 1 && !splitk_fixup<DT, T>(acc, pid, split, splits, counters, partials, lds))
-        return;
-
+// Accumulators of a finished tile to C (INT4: the sums carried times 256
+// shifted back).
+template <int DT, class T>
+__device__ __forceinline__ void pf_store(const EpiParams &epi, void *Cv,
+                                         const typename Acc<DT, T::MS>::type (&acc)[T::FM][T::FN], int tm,
+                                         int tn, int M, int N) {
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int r = lane % T::MS, h = lane / T::MS;
+    const int wm = wave / T::WGN, wn = wave % T::WGN;
     const long row0 = (long)tm * T::BM + wm * T::WTM;
     const long col0 = (long)tn * T::BN + wn * T::WTN + r;
     if constexpr (DT == S4)
         epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvShift8());
     else
         epi_store_tile<DT, T::MS, T::FM, T::FN, T::NV>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
+}
+
+//
+// Split-K (splits > 1): workgroup x computes K-range x / ntiles of tile
+// x % ntiles (the K bytes divided evenly, whole slices each), stores its
+// accumulators to its slot of `partials` in register order, and counts itself
+// in counters[tile]. The workgroup that brings the count to `splits` sums the
+// tile's partials in split order 0, 1, ... (so the result does not depend on
+// which workgroup finishes last), writes C and resets the counter to zero for
+// the next call. No workgroup waits for another. The counters must be zero
+// before the first call.
+template <int DT, class T, bool SPREAD>
+__global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_pf(const uint8_t *__restrict__ A,
+                                                               const uint8_t *__restrict__ B,
+                                                               void *__restrict__ Cv, int M,
+                                                               int N, int Kb, int tiles_m,
+                                                               int tiles_n, int splits,
+                                                               int *__restrict__ counters,
+                                                               uint32_t *__restrict__ partials,
+                                                               EpiParams epi) {
+    static_assert(T::KCH % 2 == 0, "even number of K-chunks per slice");
+    typedef typename Acc<DT, T::MS>::type acc_t;
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
+
+    const int ntiles = tiles_m * tiles_n;
+    const int split = blockIdx.x / ntiles, pid = blockIdx.x - split * ntiles;
+    int tm, tn;
+    tile_coords(pid, ntiles, tiles_m, tiles_n, T::GROUP_M, tm, tn);
+    const int KT = Kb / splits / T::BKB;  // slices of this workgroup's K-range
+
+    acc_t acc[T::FM][T::FN];
+    pf_accumulate<DT, T, SPREAD>(lds, A, B, M, N, Kb, tm, tn, split * KT, KT, acc);
+
+    if (splits > 1 && !splitk_fixup<DT, T>(acc, pid, split, splits, counters, partials, lds))
+        return;
+    pf_store<DT, T>(epi, Cv, acc, tm, tn, M, N);
 }
 
 // ---------------------------------------------------------------------------

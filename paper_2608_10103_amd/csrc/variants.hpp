@@ -15,6 +15,7 @@
 #include "wide_gemm.hpp"
 #include "wide_f6.hpp"
 #include "wide_i4.hpp"
+#include "stream_k.hpp"
 
 // Tile configurations (kernel template arguments need external linkage).
 namespace mpg {
@@ -62,7 +63,7 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5, I4WIDE = 6 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5, I4WIDE = 6, TILED_SK = 7, WIDE_SK = 8 };
 
 struct Variant {
     const char *name;
@@ -82,6 +83,8 @@ typedef void (*kernel_fn)(const uint8_t *, const uint8_t *, void *, int, int, in
                           EpiParams);
 typedef void (*splitk_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int, int,
                           int *, uint32_t *, EpiParams);
+typedef void (*sk_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int, int, SkArgs,
+                      EpiParams);
 typedef void (*generic_fn)(const uint8_t *, const uint8_t *, void *, int, int, int, int,
                            EpiParams);
 
@@ -97,6 +100,14 @@ Variant pipelined(const char *name) {
     splitk_fn f = &tiled_gemm_pf<DT, T, SPREAD>;
     return Variant{name, TILED, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
                    true};
+}
+
+// Stream-K schedule of the pipelined kernel (stream_k.hpp).
+template <int DT, class T, bool SPREAD>
+Variant pipelined_sk(const char *name) {
+    sk_fn f = &tiled_gemm_sk<DT, T, SPREAD>;
+    return Variant{name, TILED_SK, T::BM, T::BN, T::BKB, T::NTHREADS, reinterpret_cast<const void *>(f),
+                   false};
 }
 
 template <int DT, class T, int NSETS>
@@ -146,6 +157,19 @@ Variant wide(const char *name) {
 // INT4 on the FP6 cores with the conversion inside the GEMM (wide_i4.hpp);
 // bkb holds the K multiple it needs (in elements). AUX: cache policy of the
 // operand loads.
+// Stream-K schedule of the one-wave-per-SIMD kernel (stream_k.hpp); FP16
+// and INT8 only, like wide().
+template <int DT>
+Variant wide_sk(const char *name) {
+    const void *f = nullptr, *fe = nullptr;
+    if constexpr (DT == F16 || DT == S8) {
+        sk_fn k = &wide_gemm_sk<DT, true>, ke = &wide_gemm_sk<DT, false>;
+        f = reinterpret_cast<const void *>(k);
+        fe = reinterpret_cast<const void *>(ke);
+    }
+    return Variant{name, WIDE_SK, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false, fe};
+}
+
 template <int AUX = CP_DEFAULT>
 Variant i4wide(const char *name) {
     kernel_fn k = &wide_i4_gemm<true, AUX>, ke = &wide_i4_gemm<false, AUX>;
@@ -234,11 +258,14 @@ Variant generic(const char *name) {
      wide<DT>("wide256x256_w2x2_k128_m16"),                                \
      wide<DT, CP_SC0>("wide256x256_w2x2_k128_m16_sc0"),                    \
      wide<DT, CP_SC1>("wide256x256_w2x2_k128_m16_sc1"),                    \
-     wide<DT, CP_NT>("wide256x256_w2x2_k128_m16_nt")
+     wide<DT, CP_NT>("wide256x256_w2x2_k128_m16_nt"),                     \
+     wide_sk<DT>("wide256x256_w2x2_k128_m16_sk"),                          \
+     pipelined_sk<DT, T256x256_w8_s2, false>("pipe256x256_w2x4_k128_s2_sk"), \
+     pipelined_sk<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4_sk")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 54;
+constexpr int kNumCommon = 57;
 constexpr int kNumFp6 = 16;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -125,32 +125,32 @@ __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b
     });
 }
 
-// PLAIN: raw sums to the row-major output (the entry points' common case),
-// stored straight from the accumulators; otherwise the shared epilogue with
-// scales, zero points and output types (see EpiParams). AUX: cache policy
-// of the copy loads.
-template <int DT, bool PLAIN = true, int AUX = CP_DEFAULT>
-__global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t *__restrict__ A,
-                                                                 const uint8_t *__restrict__ B,
-                                                                 void *__restrict__ Cv, int M, int N, int Kb,
-                                                                 int tiles_m, int tiles_n, EpiParams epi) {
-    static_assert(DT == F16 || DT == S8, "FP16 and INT8");
+// Accumulate K-slices [kt0, kt0 + KT) of tile (tm, tn) into acc (zeroed
+// here) with the schedule above. On return every copy has landed and the
+// accumulators are safe to read; the waves may still be reading LDS, so a
+// caller that reuses the buffers for another tile needs a barrier first.
+template <int DT, int AUX>
+__device__ __forceinline__ void wide_accumulate(uint8_t *lds, const uint8_t *A, const uint8_t *B, int Kb,
+                                                int tm, int tn, int kt0, int KT,
+                                                typename Acc<DT, 16>::type (&acc)[8][8]) {
     typedef WideCfg T;
     typedef typename Acc<DT, 16>::type acc_t;
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
-    const int tid = threadIdx.x, lane = tid & 63;
+    // opaque thread id: see pf_accumulate
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane % 16, h = lane / 16;
     const int wm = wave / 2, wn = wave % 2;
-    int tm, tn;
-    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, 4, tm, tn);
 
     // wave w copies panel w: A rows [128 w, 128 w + 128) of the tile for w < 2,
-    // B rows [128 (w - 2), ...) otherwise, into copy blocks [16 w, 16 w + 16)
+    // B rows [128 (w - 2), ...) otherwise, into copy blocks [16 w, 16 w + 16);
+    // the panel starts at slice kt0
     WideCopy c;
-    c.panel = (wave < 2) ? A + ((size_t)tm * T::BM + wave * 128) * Kb
-                         : B + ((size_t)tn * T::BN + (wave - 2) * 128) * Kb;
-    c.bytes = 128 * Kb;
+    c.panel = ((wave < 2) ? A + ((size_t)tm * T::BM + wave * 128) * Kb
+                          : B + ((size_t)tn * T::BN + (wave - 2) * 128) * Kb) +
+              (size_t)kt0 * T::BKB;
+    c.bytes = 128 * Kb - kt0 * T::BKB;
     c.voff = (uint32_t)((lane / 8) * 16 * Kb + (lane % 8) * 16);
     c.kb = Kb;
     c.dst = lds + wave * 16 * T::BLK;
@@ -159,7 +159,6 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     const uint8_t *ra0 = lds + (wm * 16 + r) * T::BLK + h * 16;
     const uint8_t *rb0 = lds + (32 + wn * 16 + r) * T::BLK + h * 16;
 
-    acc_t acc[8][8];
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -175,7 +174,6 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
         for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
     asm volatile("s_nop 4" ::: "memory");
 
-    const int KT = Kb / T::BKB;
     // prologue: slice 0 whole, loads 0-11 of slice 1; wait for slice 0
 #pragma unroll
     for (int j = 0; j < 16; ++j) wide_load<AUX>(c, j, 0, 0);
@@ -211,7 +209,19 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) asm volatile("" : "+a"(acc[i][j]));
+}
 
+// Accumulators of a finished tile to C. PLAIN: raw sums of a whole tile to
+// the row-major output, stored straight from the accumulators; otherwise the
+// shared epilogue with scales, zero points and output types (see EpiParams).
+template <int DT, bool PLAIN>
+__device__ __forceinline__ void wide_store(const EpiParams &epi, void *Cv,
+                                           const typename Acc<DT, 16>::type (&acc)[8][8], int tm, int tn,
+                                           int M, int N) {
+    typedef WideCfg T;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane % 16, h = lane / 16;
+    const int wm = wave / 2, wn = wave % 2;
     const long row0 = (long)tm * T::BM + wm * 128;
     const long col0 = (long)tn * T::BN + wn * 128 + r;
     if constexpr (PLAIN) {
@@ -230,6 +240,21 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     } else {
         epi_store_tile<DT, 16, 8, 8, 4>(epi, Cv, acc, row0, col0, h, M, N, ConvSame());
     }
+}
+
+// PLAIN: see wide_store. AUX: cache policy of the copy loads.
+template <int DT, bool PLAIN = true, int AUX = CP_DEFAULT>
+__global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t *__restrict__ A,
+                                                                 const uint8_t *__restrict__ B,
+                                                                 void *__restrict__ Cv, int M, int N, int Kb,
+                                                                 int tiles_m, int tiles_n, EpiParams epi) {
+    static_assert(DT == F16 || DT == S8, "FP16 and INT8");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[WideCfg::LDS_BYTES];
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, 4, tm, tn);
+    typename Acc<DT, 16>::type acc[8][8];
+    wide_accumulate<DT, AUX>(lds, A, B, Kb, tm, tn, 0, Kb / WideCfg::BKB, acc);
+    wide_store<DT, PLAIN>(epi, Cv, acc, tm, tn, M, N);
 }
 
 }  // namespace mpg

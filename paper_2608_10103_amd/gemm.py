@@ -67,6 +67,9 @@ def lib() -> ctypes.CDLL:
     L.mpgemm_run_variant.restype = I
     L.mpgemm_select_splits.argtypes = [I, I, I, I, I]
     L.mpgemm_select_splits.restype = I
+    IP = ctypes.POINTER(ctypes.c_int)
+    L.mpgemm_sk_schedule.argtypes = [I, I, I, I, I, IP, IP, IP]
+    L.mpgemm_sk_schedule.restype = I
     L.gemm_scaled.argtypes = [I, I, I, I, P, P, P, P, P]
     L.gemm_scaled.restype = I
     S = ctypes.c_size_t
@@ -94,7 +97,7 @@ EXPORTED_SYMBOLS = ("gemm_f16_f32", "gemm_s8_s32", "gemm_s4_s32", "gemm_scaled",
                     "mpgemm_select_variant", "mpgemm_select_variant_ws", "mpgemm_variant_supports",
                     "mpgemm_run_variant",
                     "mpgemm_select_splits", "mpgemm_run_variant_ws", "mpgemm_s4_run_to_fp6",
-                    "mpgemm_s4_run_to_e2m3", "mpgemm_gemm_bt")
+                    "mpgemm_s4_run_to_e2m3", "mpgemm_gemm_bt", "mpgemm_sk_schedule")
 
 
 def _stream_ptr(stream, device) -> int:
@@ -318,6 +321,17 @@ def raw_call(dtype: str, M: int, N: int, K: int, a_ptr: int, b_ptr: int, c_ptr: 
 def select_splits(dtype: str, variant: int, M: int, N: int, K: int) -> int:
     """Split-K count the entry points use for this variant (1 = none)."""
     return lib().mpgemm_select_splits(DTYPE_CODE[dtype], variant, M, N, K)
+
+
+def sk_schedule(dtype: str, variant: int, M: int, N: int, K: int) -> tuple[int, int, int]:
+    """Stream-K schedule of a variant for this problem on the current device:
+    (whole tiles first, K-parts of each remaining tile (1: off), grid)."""
+    dp, parts, grid = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    code = lib().mpgemm_sk_schedule(DTYPE_CODE[dtype], variant, M, N, K, ctypes.byref(dp),
+                                    ctypes.byref(parts), ctypes.byref(grid))
+    if code != 0:
+        raise HipError(code, f"stream-K schedule of {dtype} variant {variant} for {M}x{N}x{K}")
+    return dp.value, parts.value, grid.value
 
 
 def num_variants(dtype: str) -> int:

@@ -67,7 +67,7 @@ def main(argv=None) -> int:
                 name = mp.variant_name(dt, v)
                 if v == 0 and M * N * K > 1024 ** 3:
                     continue
-                if want and not any(w in name for w in want):
+                if want and not any((name == w[1:]) if w.startswith("=") else (w in name) for w in want):
                     continue
                 if not mp.variant_supports(dt, v, M, N, K, Ad.data_ptr(), Bd.data_ptr()):
                     continue

@@ -544,8 +544,9 @@ def test_s4_4096_in_a_hip_graph():
 
 
 def _pipelined_variants(dtype):
+    """The variants that split K (the stream-K ones do not)."""
     return [v for v in range(mp.num_variants(dtype))
-            if mp.variant_name(dtype, v).startswith(("pipe", "spread"))]
+            if mp.variant_name(dtype, v).startswith(("pipe", "spread")) and not mp.variant_name(dtype, v).endswith("_sk")]
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
@@ -575,7 +576,9 @@ def test_llm_inference_shapes(dtype):
     for (M, N, K) in [(1, 4096, 4096), (16, 4096, 4096), (64, 8192, 4096), (128, 4096, 8192),
                       (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048),
                       # the narrow tiles, mirrored when N is the small side
-                      (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024)]:
+                      (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024),
+                      # 272 tiles of 128 x 128: stream-K with a workspace
+                      (2100, 2000, 6400)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
         ref = oracle_gemm(dtype, A, B)
         v = mp.select_variant(dtype, M, N, K)
@@ -633,6 +636,82 @@ def test_splitk_argument_errors():
     assert run(v, 16, 1024, ws.data_ptr(), 4096) == INVALID  # too small for it
     assert run(v, 16, 1024) == 0
     torch.cuda.synchronize()
+
+
+# ---------------------------------------------------------------- stream-K
+
+
+def _named(dtype, name):
+    return [v for v in range(mp.num_variants(dtype)) if mp.variant_name(dtype, v) == name][0]
+
+
+SK_WIDE, SK_PIPE, SK_SPREAD = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk",
+                               "spread128x128_w2x2_k128_s4_sk")
+# tile counts just past one or two rounds of 256 workgroups (one per CU),
+# K deep enough for the schedule to split the remaining tiles
+SK_CASES = [
+    ("f16", SK_WIDE, 4352, 4096, 4096),    # 272 tiles: 256 whole, 16 in 4 parts
+    ("s8", SK_WIDE, 6144, 6400, 8192),     # 600 = 2 x 256 + 88 tiles, 2 parts
+    ("f16", SK_WIDE, 2048, 2048, 8192),    # 64 tiles, all split
+    ("s8", SK_WIDE, 4352, 4096, 6400),     # 50 slices in 3 parts of 16 or 17
+    ("f16", SK_PIPE, 4000, 4400, 3200),    # ragged edges, 288 tiles
+    ("s8", SK_PIPE, 4000, 4400, 6400),
+    ("s4", SK_PIPE, 4000, 4400, 12800),
+    ("f16", SK_SPREAD, 2100, 2000, 3200),  # 272 tiles of 128 x 128
+    ("s8", SK_SPREAD, 128 * 16 + 5, 128 * 16, 8192),
+    ("s4", SK_SPREAD, 2100, 2000, 12800),
+    ("s4", SK_SPREAD, 128 * 23 + 5, 128 * 12, 16384),
+]
+
+
+@pytest.mark.parametrize("dtype,name,M,N,K", SK_CASES, ids=[f"{c[0]}-{c[1][:6]}-{c[2]}x{c[3]}x{c[4]}" for c in SK_CASES])
+def test_stream_k_parity(dtype, name, M, N, K):
+    """Stream-K variants where their schedule splits tiles into K-parts:
+    every 13th row (and the last) against the oracle (bit-exact integers,
+    FP16 within the bound), four launches on one workspace bit-identical
+    (the sum does not depend on which part finishes last), the counter block
+    left zero, and the same variant without a workspace (every tile whole):
+    integers bit-identical over the whole output, FP16 on the sampled rows."""
+    v = _named(dtype, name)
+    dp, parts, grid = mp.sk_schedule(dtype, v, M, N, K)
+    _log(f"stream-K {dtype} {name} {M}x{N}x{K}: {dp} whole tiles, then {parts} parts per tile, grid {grid}")
+    assert parts > 1
+    A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
+    Ad, Bd = dev(A), dev(B)
+    ws = mp.new_workspace(mp.workspace_size(dtype, M, N, K, variant=v, splits=1), "cuda")
+    C = mp.GEMM[dtype](Ad, Bd, variant=v, workspace=ws)
+    for _ in range(3):
+        assert torch.equal(C, mp.GEMM[dtype](Ad, Bd, variant=v, workspace=ws))
+    whole = mp.GEMM[dtype](Ad, Bd, variant=v)
+    torch.cuda.synchronize()
+    assert int(ws[:65536].count_nonzero()) == 0, "counters left non-zero"
+    rows = np.array(sorted(set(range(0, M, 13)) | {M - 1}))
+    ref = oracle_gemm(dtype, A, B, rows=rows)
+    assert_parity(dtype, C.cpu().numpy()[rows], *ref, f"stream-K {dtype} {name} {M}x{N}x{K}")
+    if dtype == "f16":
+        assert_parity(dtype, whole.cpu().numpy()[rows], *ref, f"whole tiles {dtype} {name} {M}x{N}x{K}")
+    else:
+        assert torch.equal(C, whole)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_stream_k_scaled(dtype):
+    """The scaled epilogue (and zero points for integers) through stream-K
+    on the one-wave-per-SIMD kernel (FP16, INT8) and the 128 x 128 one."""
+    cases = [(SK_SPREAD, 2100, 2000, {"f16": 3200, "s8": 6400, "s4": 12800}[dtype])]
+    if dtype != "s4":
+        cases.append((SK_WIDE, 2048, 2048, {"f16": 4096, "s8": 8192}[dtype]))
+    for i, (name, M, N, K) in enumerate(cases):
+        v = _named(dtype, name)
+        assert mp.sk_schedule(dtype, v, M, N, K)[1] > 1
+        out = OUTS[i % 3]
+        zp = dtype != "f16"
+        A, B = si.gen_operands(dtype, M, N, K, seed=2100 + i)
+        sa, sb, za, zb = _scales(dtype, M, N, 2200 + i, zp)
+        _log(f"stream-K scaled {dtype} {name} {M}x{N}x{K} {out}")
+        C = _run_scaled(dtype, A, B, out, sa, sb, za, zb, variant=v)
+        _, exact, D = oracle.gemm_scaled(dtype, A, B, out, sa, sb, za, zb)
+        assert_scaled(C, exact, D, out, f"stream-K {dtype} {name} {M}x{N}x{K} {out} zp={zp}")
 
 
 # ---------------------------------------------------------------- scaled outputs (fused epilogue)

@@ -1,0 +1,141 @@
+"""Host-side checks of the stream-K schedule (no GPU): the plan the library
+reports (mpgemm_sk_schedule) computes every (tile, K-slice) iteration
+exactly once: whole tiles first, then the remaining tiles cut into K-parts
+as the kernels cut them (sk_work), one workgroup and one partial slot each.
+Without a visible device the library plans for 256 resident workgroups (one
+per MI355X CU)."""
+import ctypes
+import math
+import re
+
+import pytest
+
+import paper_2608_10103_amd as mp
+
+G = 256
+SK_NAMES = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk", "spread128x128_w2x2_k128_s4_sk")
+BYTES_PER_ELEM = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
+
+
+def _variant(dtype, name):
+    return [v for v in range(mp.num_variants(dtype)) if mp.variant_name(dtype, v) == name][0]
+
+
+def _tile(name):
+    return tuple(int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
+
+
+def _work(b, dp, parts, KT):
+    """(tile, first slice, slices, slot) of workgroup b; the whole-tile
+    workgroups' tiles are a permutation of 0 .. dp - 1 (XCD-contiguous), so
+    only their count matters here."""
+    if b < dp:
+        return None
+    u = b - dp
+    j = u % parts
+    k0, k1 = j * KT // parts, (j + 1) * KT // parts
+    return dp + u // parts, k0, k1 - k0, u
+
+
+CASES = [  # dtype, name, M, N, K
+    ("f16", SK_NAMES[0], 4352, 4096, 4096),      # 272 tiles: 256 whole, 16 split, 64 slices: 4 parts
+    ("f16", SK_NAMES[0], 4352, 4096, 8192),      # 128 slices: 5 parts
+    ("s8", SK_NAMES[0], 4352, 4096, 8192),       # 64 slices
+    ("s8", SK_NAMES[0], 4352, 4096, 4096),       # 32 slices: no gain expected, off
+    ("s8", SK_NAMES[0], 6144, 6400, 16384),      # 600 = 2 x 256 + 88: at most 2 parts
+    ("s8", SK_NAMES[0], 256 * 3, 256 * 86, 65536),  # 258 tiles, 512 slices: capped at 8
+    ("f16", SK_NAMES[0], 2048, 2048, 8192),      # 64 tiles, fewer than the CUs
+    ("f16", SK_NAMES[1], 4000, 4400, 6400),      # ragged, 288 tiles, 100 slices
+    ("s4", SK_NAMES[1], 4000, 4400, 25600),
+    ("s8", SK_NAMES[2], 2100, 2000, 8192),       # 272 tiles of 128 x 128
+    ("s4", SK_NAMES[2], 128 * 23 + 5, 128 * 12, 32768),
+    ("f16", SK_NAMES[2], 128 * 16 + 1, 128 * 16, 128 * 3),  # 3 slices: off
+]
+
+
+@pytest.mark.parametrize("dtype,name,M,N,K", CASES)
+def test_sk_schedule_covers_every_iteration_once(dtype, name, M, N, K):
+    v = _variant(dtype, name)
+    bm, bn = _tile(name)
+    tiles = -(-M // bm) * -(-N // bn)
+    KT = int(K * BYTES_PER_ELEM[dtype]) // 128
+    dp, parts, grid = mp.sk_schedule(dtype, v, M, N, K)
+    q, r = divmod(tiles, G)
+    # the library's cost model: s = round(sqrt(KT / 5)) capped at G / r and
+    # 8, taken when KT (1 - 1/s) - 5 (s - 1) - 13 exceeds KT / 10
+    want_parts = min(int(math.sqrt(KT / 5) + 0.5), G // r, 8) if r and 2 * r <= G else 1
+    gain = KT * (1 - 1 / want_parts) - 5 * (want_parts - 1) - 13 if want_parts >= 2 else 0
+    if want_parts < 2 or gain <= KT / 10:
+        assert (dp, parts, grid) == (tiles, 1, tiles)
+        return
+    assert (dp, parts, grid) == (q * G, want_parts, q * G + r * want_parts)
+    assert grid - dp <= G, "the split remainder fits one round"
+    covered = {t: [] for t in range(dp, tiles)}
+    slots = set()
+    for b in range(grid):
+        w = _work(b, dp, parts, KT)
+        if w is None:
+            continue
+        t, k0, n, u = w
+        assert n >= KT // parts and u not in slots
+        slots.add(u)
+        covered[t].append((k0, n))
+    for t, ps in covered.items():
+        assert len(ps) == parts
+        assert sorted(ps)[0][0] == 0
+        assert all(a[0] + a[1] == b[0] for a, b in zip(sorted(ps), sorted(ps)[1:])), f"tile {t} parts not contiguous"
+        assert sum(n for _, n in ps) == KT
+    assert slots == set(range(grid - dp))
+    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == 65536 + (grid - dp) * bm * bn * 4
+
+
+@pytest.mark.parametrize("dtype,name,M,N,K", [
+    ("f16", SK_NAMES[0], 4096, 4096, 512),        # 256 tiles: one full round
+    ("s8", SK_NAMES[0], 8192, 8192, 1024),        # 1024 tiles: whole rounds
+    ("f16", SK_NAMES[1], 4000, 8000, 512),        # 16 x 32 = 512 tiles
+    ("s8", SK_NAMES[0], 256 * 20, 256 * 20, 1024),  # 400 = 256 + 144: last round over half full
+    ("s4", SK_NAMES[2], 2048, 2048, 512),         # 256 tiles
+    ("s8", "pipe256x256_w2x4_k128_s2", 4352, 4096, 1024),  # not a stream-K variant
+])
+def test_sk_schedule_off(dtype, name, M, N, K):
+    """Whole rounds, a last round over half full, or a variant without the
+    schedule: every tile whole, one workgroup each, and no workspace."""
+    v = _variant(dtype, name)
+    bm, bn = _tile(name)
+    tiles = -(-M // bm) * -(-N // bn)
+    assert mp.sk_schedule(dtype, v, M, N, K) == (tiles, 1, tiles)
+    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == 0
+
+
+def test_sk_schedule_errors():
+    L = mp.lib()
+    x = ctypes.c_int()
+    p = ctypes.byref(x)
+    v = _variant("f16", SK_NAMES[0])
+    assert L.mpgemm_sk_schedule(0, v, 4352, 4096, 512, None, p, p) == 1
+    assert L.mpgemm_sk_schedule(0, -1, 4352, 4096, 512, p, p, p) == 1
+    assert L.mpgemm_sk_schedule(7, v, 4352, 4096, 512, p, p, p) == 1
+    # the one-wave-per-SIMD kernel needs whole tiles; it has no INT4 kernel
+    assert L.mpgemm_sk_schedule(0, v, 4353, 4096, 512, p, p, p) == 1
+    assert L.mpgemm_sk_schedule(2, _variant("s4", SK_NAMES[0]), 4352, 4096, 512, p, p, p) == 1
+
+
+def test_sk_selection_with_a_workspace():
+    """With a workspace the automatic choice takes the stream-K twin of the
+    kernel it would pick where that twin's schedule is on; without one, or
+    where the schedule is off, the whole-tile kernel."""
+    name = lambda d, M, N, K, ws: mp.variant_name(d, mp.select_variant(d, M, N, K, with_ws=ws))
+    for d, M, N, K, plain, twin in [
+        ("f16", 4352, 4096, 8192, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
+        ("s8", 4352, 4096, 16384, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
+        ("f16", 4000, 4400, 6400, "pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2_sk"),
+        ("s8", 2100, 2000, 6400, "spread128x128_w2x2_k128_s4", "spread128x128_w2x2_k128_s4_sk"),
+        ("s4", 2100, 2000, 12800, "spread128x128_w2x2_k128_s4", "spread128x128_w2x2_k128_s4_sk"),
+    ]:
+        assert name(d, M, N, K, False) == plain, (d, M, N, K)
+        assert name(d, M, N, K, True) == twin, (d, M, N, K)
+    # schedule off: too few slices, whole rounds, last round over half full
+    for d, M, N, K in [("s8", 4352, 4096, 4096), ("f16", 8192, 8192, 8192), ("f16", 5120, 5120, 8192)]:
+        assert not name(d, M, N, K, True).endswith("_sk"), (d, M, N, K)
+    # INT4 with a workspace keeps the FP6 pre-pass kernel (no stream-K twin)
+    assert name("s4", 4352, 4096, 16384, True) == "fp6wide256x256_w2x2_k128_s3"
