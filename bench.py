@@ -134,6 +134,9 @@ def main():
                          "script's runs over --points: mfma= (SQ_VALU_MFMA_BUSY_CYCLES, SQ_WAVES, "
                          "SQ_WAVE_CYCLES, SQ_LDS_BANK_CONFLICT, GRBM_GUI_ACTIVE), fetch= (FETCH_SIZE), "
                          "write= (WRITE_SIZE), copyfetch= and copywrite= (the same of a --copy-mib run)")
+    ap.add_argument("--write-traffic", action="store_true",
+                    help="with --counters-table: store every point's HBM-side traffic per launch in "
+                         "profiles/traffic.json")
     args = ap.parse_args()
 
     if args.ingest_pmc:
@@ -453,6 +456,7 @@ def counters_table(args):
             vals = [c[cname] for _, c, _ in _dispatches_any(folders[kind]) if cname in c]
             scale[cname] = float(np.median(vals)) / (args.copy_mib_ref * 1024.0)
     med = lambda xs: float(np.median(xs)) if xs else float("nan")
+    traffic, prepass = {}, {}
     print("| point | kernel | median us | clock GHz | MFMA busy | waves/SIMD | LDS conflicts per CU-cycle | "
           "FETCH KiB | WRITE KiB | HBM-side MB | HBM GB/s | algorithmic MB | traffic / algorithmic |")
     print("|---|---|---|---|---|---|---|---|---|---|---|---|---|")
@@ -482,9 +486,23 @@ def counters_table(args):
         alg = 2 * n * n * elem + 4.0 * n * n if role != "pre-pass" else 2 * n * n * 0.5 + 2 * n * n * 0.75
         kname = slot["kernel"].split("(")[0].replace("void ", "")
         label = f"{dt} {n}" + (" (pre-pass)" if role == "pre-pass" else "")
+        if role == "pre-pass":
+            prepass[i] = hbm
+        else:
+            traffic[f"{dt}:{n}:{role}"] = {"kernel_source_hash": kernel_source_hash(role), "kernel_name": kname,
+                                           "fetch_kib_per_launch": fk, "write_kib_per_launch": wk,
+                                           "hbm_bytes_per_launch": int(hbm)}
+            if i in prepass:
+                traffic[f"{dt}:{n}:{role}"]["prepass_hbm_bytes_per_launch"] = int(prepass[i])
         print(f"| {label} | `{kname}` | {dur_ns / 1e3:.1f} | {clock:.2f} | {100 * mfma:.1f}% | {waves:.2f} | "
               f"{lds:.4f} | {fk:.0f} | {wk:.0f} | {hbm / 1e6:.1f} | {hbm / dur_ns:.0f} | {alg / 1e6:.1f} | "
               f"{hbm / alg:.2f} |")
+    if args.write_traffic:
+        out = {"copy_calibration": {"mib": args.copy_mib_ref, "fetch_scale": scale["FETCH_SIZE"],
+                                    "write_scale": scale["WRITE_SIZE"]},
+               "points": traffic}
+        os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+        json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
 
 
 def _dispatches_any(folder):
