@@ -177,9 +177,10 @@ hipError_t mpgemm_gemm_ws(int dtype, int M, int N, int K, const void *A, const v
  * a caller workspace. Allocates and frees nothing. The first call on a
  * device looks up that device's array address (hipGetSymbolAddress). The
  * automatic choice is the one mpgemm_gemm_ws makes with a 32 MiB workspace: a
- * split that would need more is not taken; zero points needing more
- * (M + N above about 8.4 million) return hipErrorInvalidValue. A split call
- * first clears the tile counters with a small kernel on `stream`. Every
+ * split or stream-K schedule (or the INT4 pre-pass) that would need more is
+ * not taken; zero points needing more (M + N above about 8.4 million) return
+ * hipErrorInvalidValue. A split or stream-K call first clears the tile
+ * counters with a small kernel on `stream`. Every
  * call on a device shares that device's array: calls that may overlap on
  * one device (other streams, other threads) race, and must be ordered by
  * the caller (one stream, or events). Other arguments, semantics and errors

@@ -2,8 +2,9 @@
 through the C ABI, against the workspace entry point it mirrors
 (mpgemm_gemm_ws with a caller workspace) and the CPU oracle: two calls in a
 row, the second on a smaller problem, with no synchronisation between them;
-split-K shapes (the scratch holds the partial tiles and the counters, cleared
-by the call) and zero points (the scratch holds the row sums)."""
+split-K and stream-K shapes (the scratch holds the partial tiles and the
+counters, cleared by the call) and zero points (the scratch holds the row
+sums)."""
 import ctypes
 
 import numpy as np
@@ -59,6 +60,33 @@ def test_noalloc_matches_the_workspace_entry_point(dtype, shapes):
         assert _with_ws(dtype, Ad, Bd, ref, M, N, K) == 0
         assert torch.equal(C, ref), (dtype, M, N, K)  # same kernel, same split, same order
         assert_parity(dtype, C.cpu().numpy(), *oracle_gemm(dtype, A, B), f"noalloc {dtype} {M}x{N}x{K}")
+
+
+@pytest.mark.parametrize("dtype", ["f16", "s8"])
+def test_noalloc_stream_k(dtype):
+    """Stream-K shapes (the scratch holds the split tiles' partials and the
+    tile counters): two calls in a row, the second smaller with another
+    schedule, against mpgemm_gemm_ws and the oracle."""
+    shapes = [(2100, 2000, 6400), (1200, 1100, 4096)] if dtype == "f16" else [(2100, 2000, 12800), (1200, 1100, 8192)]
+    ops, outs = [], []
+    for i, (M, N, K) in enumerate(shapes):
+        v = mp.select_variant(dtype, M, N, K, with_ws=True)
+        assert mp.variant_name(dtype, v).endswith("_sk") and mp.sk_schedule(dtype, v, M, N, K)[1] > 1
+        assert mp.workspace_size(dtype, M, N, K) <= 32 << 20
+        A, B = si.gen_operands(dtype, M, N, K, seed=4300 + i)
+        Ad, Bd = dev(A), dev(B)
+        C = torch.full((M, N), -7, dtype=OUT[dtype], device="cuda")
+        assert _noalloc(dtype, Ad, Bd, C, M, N, K) == 0
+        ops.append((A, B, Ad, Bd, M, N, K))
+        outs.append(C)
+    torch.cuda.synchronize()
+    for (A, B, Ad, Bd, M, N, K), C in zip(ops, outs):
+        ref = torch.full((M, N), -9, dtype=OUT[dtype], device="cuda")
+        assert _with_ws(dtype, Ad, Bd, ref, M, N, K) == 0
+        assert torch.equal(C, ref), (dtype, M, N, K)
+        rows = np.array(sorted(set(range(0, M, 7)) | {M - 1}))
+        assert_parity(dtype, C.cpu().numpy()[rows], *oracle_gemm(dtype, A, B, rows=rows),
+                      f"noalloc stream-K {dtype} {M}x{N}x{K}")
 
 
 def test_noalloc_zero_points():
