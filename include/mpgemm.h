@@ -256,24 +256,30 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
 int mpgemm_select_splits(int dtype, int variant, int M, int N, int K);
 
 /* Stream-K: the variants named "..._sk" (the one-wave-per-SIMD FP16/INT8
- * kernel, the 256x256 and the 128x128 pipelined kernels) share the last,
- * partly filled round of a problem's tiles out over more workgroups. With T
- * tiles, G workgroups resident at once (one per CU: 256 on MI355X) and
- * T = q G + r, 0 < r <= G / 2: workgroups 0 .. q G - 1 compute one whole tile
- * each; the K-slices (KT per tile, 128 bytes of K each) of each of the r
- * remaining tiles are then cut into s contiguous parts, one workgroup each,
- * s = round(sqrt(KT / 5)) capped at G / r and 8. The last of a tile's parts
- * to finish adds the s partial tiles in part order and writes C, so results
- * do not depend on scheduling (FP16: the order of summation differs from
- * the whole-tile kernel's, within the same error bound; integers: exact).
+ * kernel, the 256x256 and the 128x128 pipelined kernels, and the INT4
+ * one-wave-per-SIMD FP6 kernel fed by the conversion pre-pass) share the
+ * last, partly filled round of a problem's tiles out over more workgroups.
+ * With T tiles, G workgroups resident at once (one per CU: 256 on MI355X)
+ * and T = q G + r, 0 < r <= G / 2: workgroups 0 .. q G - 1 compute one whole
+ * tile each; the K-slices (KT per tile: 128 bytes of K each, or 128 k of K
+ * padded to 256 for the FP6 kernel) of each of the r remaining tiles are
+ * then cut into s contiguous parts, one workgroup each, s =
+ * round(sqrt(KT t / 5)) capped at G / r, 8 and KT / 2, where t is the time
+ * of a slice in microseconds (1; 0.5 for the FP6 kernel). The last of a
+ * tile's parts to finish adds the s partial tiles in part order and writes
+ * C, so results do not depend on scheduling (FP16: the order of summation
+ * differs from the whole-tile kernel's, within the same error bound;
+ * integers: exact, the FP6 kernel's FP32 part sums included, whose
+ * magnitudes add up to at most 64 K < 2^24).
  * Scratch, in the workspace: the 64 KiB counter block (one counter per
- * tile, left zero by every call), then r * s partial tiles of 4 x BM x BN
- * bytes. Every tile is computed whole (no scratch) without a large enough
- * workspace, when T is a multiple of G, r > G / 2, T is beyond 16384 tiles,
- * s < 2, or the expected gain, KT (1 - 1/s) - 5 (s - 1) - 13 slice-times,
- * is at most KT / 10. With a workspace the automatic choice takes a
- * stream-K variant in place of its whole-tile kernel where its schedule is
- * on.
+ * tile, left zero by every call), then (after the FP6 kernel's converted
+ * operands) r * s partial tiles of 4 x BM x BN bytes. Every tile is computed
+ * whole without a large enough workspace, when T is a multiple of G,
+ * r > G / 2, T is beyond 16384 tiles, s < 2, or the expected gain,
+ * KT t (1 - 1/s) - 5 (s - 1) - 13 microseconds, is at most KT t / 10 (a
+ * quarter of KT t for the FP6 kernel). With a workspace the automatic
+ * choice takes a stream-K variant in place of its whole-tile kernel where
+ * its schedule is on and its scratch fits, else the whole-tile kernel.
  * mpgemm_sk_schedule: the schedule a stream-K variant would use for this
  * problem on the current device (G = 256 when no device is visible):
  * *dp_tiles whole tiles first, then *parts parts per remaining tile (1:

@@ -108,13 +108,13 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
         if (kb % v.bkb || 128 * kb > INT_MAX) return false;
         return aligned(A, 16) && aligned(B, 16);
     }
-    if (v.kind == FP6 || v.kind == FP6WIDE) {
-        if (dtype != S4) return false;
+    if (v.kind == FP6 || v.kind == FP6WIDE || v.kind == FP6WIDE_SK) {
+        if (dtype != S4 || !v.fn) return false;
         if (F6Geom::runs_pad(K) * 32 > kF6MaxK) return false;
         if (F6Geom::rows_pad(M) > kF6MaxRows || F6Geom::rows_pad(N) > kF6MaxRows) return false;
         // the one-wave-per-SIMD kernel addresses each workspace part (P: 16
         // bytes per row and run) with 32-bit byte offsets
-        if (v.kind == FP6WIDE)
+        if (v.kind == FP6WIDE || v.kind == FP6WIDE_SK)
             return F6Geom::runs_pad(K) * 16 * (F6Geom::rows_pad(M) > F6Geom::rows_pad(N) ? F6Geom::rows_pad(M)
                                                                                           : F6Geom::rows_pad(N)) <= INT_MAX;
         return true;
@@ -171,17 +171,20 @@ int resident_groups() {
 // or the last round more than half, beyond the counter block, or where the
 // cost model below expects no gain.
 //
-// Cost model, in units of one K-slice of one tile (about 1 us for a 256 x
-// 256 tile on MI355X, FP16 and INT8 alike, and proportionally less for
-// 128 x 128 tiles, whose partials are proportionally smaller): a tile's
-// last-round time without stream-K is KT slices; with s parts it is KT / s,
-// plus about 5 per partial tile the finishing part loads (s - 1; one
-// workgroup reads them at about 50 GB/s) and about 13 for publishing,
-// fencing and counting (timelines of the kernels at 4352 x 4096 x
-// {4096, 8192}). Gain(s) = KT (1 - 1/s) - 5 (s - 1) - 13 peaks near
-// s = sqrt(KT / 5); stream-K is taken when that gain exceeds a tenth of KT
-// (K-ranges of about 48 slices and more: FP16 K >= 3072, INT8 K >= 6144 with
-// 256 x 256 tiles).
+// Cost model, in microseconds (timelines of the kernels at 4352 x 4096 x
+// {4096, 8192} on MI355X): a remainder tile's time without stream-K is
+// KT t (KT K-slices of t each: t about 1 us for a 256 x 256 tile, FP16 and
+// INT8 alike, proportionally less for 128 x 128 tiles, whose partials are
+// proportionally smaller; about 0.5 us for the FP6 kernel's 128-k slices);
+// with s parts it is KT t / s, plus about 5 per partial tile the finishing
+// part loads (s - 1; one workgroup reads them at about 50 GB/s) and about
+// 13 for publishing, fencing and counting. Gain(s) = KT t (1 - 1/s) -
+// 5 (s - 1) - 13 peaks near s = sqrt(KT t / 5); stream-K is taken when that
+// gain exceeds a tenth of KT t (K-ranges of about 48 slices and more: FP16
+// K >= 3072, INT8 K >= 6144 with 256 x 256 tiles), a quarter for the FP6
+// kernel (interleaved timings of both schedules at 6 INT4 shapes: gains
+// of 9% at 4352 x 4096 x 16384 and 6% at 2048 x 2048 x 16384, losses of up
+// to 4% where a tenth was cleared and a quarter is not).
 struct SkPlan {
     bool on;
     int dp_tiles, parts, grid;
@@ -189,7 +192,7 @@ struct SkPlan {
 
 constexpr int kSkMaxParts = 8;
 
-bool is_sk(const Variant &v) { return v.kind == TILED_SK || v.kind == WIDE_SK; }
+bool is_sk(const Variant &v) { return v.kind == TILED_SK || v.kind == WIDE_SK || v.kind == FP6WIDE_SK; }
 
 SkPlan sk_off(long tiles) { return SkPlan{false, (int)tiles, 1, (int)tiles}; }
 
@@ -198,13 +201,19 @@ SkPlan sk_plan(int dtype, const Variant &v, int M, int N, int K) {
     if (!is_sk(v) || tiles > kSplitCounters) return sk_off(tiles);
     const long G = resident_groups(), r = tiles % G;
     if (r == 0 || 2 * r > G) return sk_off(tiles);
-    const long KT = row_bytes(dtype, K) / v.bkb;
-    long parts = (long)(sqrt((double)KT / 5.0) + 0.5);
+    // slices per tile (the FP6 kernel: 128-k slices of the padded K), the
+    // time of a lone remainder tile's slice in microseconds, and the margin
+    // the modelled gain must clear (a fraction of the remainder round)
+    const bool f6 = v.kind == FP6WIDE_SK;
+    const long KT = f6 ? F6Geom::runs_pad(K) / v.bkb : row_bytes(dtype, K) / v.bkb;
+    const double t = f6 ? 0.5 : 1.0, margin = f6 ? 0.25 : 0.1;
+    long parts = (long)(sqrt(KT * t / 5.0) + 0.5);
     if (parts > G / r) parts = G / r;
     if (parts > kSkMaxParts) parts = kSkMaxParts;
+    if (parts > KT / 2) parts = KT / 2;  // at least two slices per part
     if (parts < 2) return sk_off(tiles);
-    const double gain = KT * (1.0 - 1.0 / parts) - 5.0 * (parts - 1) - 13.0;
-    if (gain <= 0.1 * KT) return sk_off(tiles);
+    const double gain = KT * t * (1.0 - 1.0 / parts) - 5.0 * (parts - 1) - 13.0;
+    if (gain <= margin * KT * t) return sk_off(tiles);
     const long dp = tiles - r;
     return SkPlan{true, (int)dp, (int)parts, (int)(dp + r * parts)};
 }
@@ -259,16 +268,35 @@ enum : int {
 // list.
 constexpr int V_WIDE_SK = kNumCommon - 3, V_PIPE256_SK = kNumCommon - 2, V_SPREAD128_SK = kNumCommon - 1;
 
-int sk_twin(int variant) {
-    return variant == V_WIDE ? V_WIDE_SK
-                             : (variant == V_PIPE256_W2X4 ? V_PIPE256_SK
-                                                          : (variant == V_SPREAD128_K128 ? V_SPREAD128_SK : -1));
-}
-
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumCommon + 1;  // fp6pipe256x256_w2x4_k128_s2
 constexpr int V_FP6_WIDE = kNumCommon + 8;    // fp6wide256x256_w2x2_k128_s3
 constexpr int V_I4WIDE = kNumCommon + 9;      // e2m3wide256x256_w2x2_k256
+constexpr int V_FP6_WIDE_SK = kNumCommon + 16;  // fp6wide256x256_w2x2_k128_s3_sk
+
+// The stream-K twin of a variant (the same kernel with the stream-K
+// schedule), or -1. The FP6 indices exist only in the INT4 table, where the
+// INT4 preferences are the only callers that name them.
+int sk_twin(int variant) {
+    switch (variant) {
+        case V_WIDE: return V_WIDE_SK;
+        case V_PIPE256_W2X4: return V_PIPE256_SK;
+        case V_SPREAD128_K128: return V_SPREAD128_SK;
+        case V_FP6_WIDE: return V_FP6_WIDE_SK;
+        default: return -1;
+    }
+}
+
+// The variant a stream-K twin schedules differently, or -1.
+int sk_base(int variant) {
+    switch (variant) {
+        case V_WIDE_SK: return V_WIDE;
+        case V_PIPE256_SK: return V_PIPE256_W2X4;
+        case V_SPREAD128_SK: return V_SPREAD128_K128;
+        case V_FP6_WIDE_SK: return V_FP6_WIDE;
+        default: return -1;
+    }
+}
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
 // taken when it supports the problem and yields at least `min_tiles`
@@ -416,11 +444,13 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     return 0;
 }
 
-// Caller workspace. Layout: [0, 64 KiB) the split-K tile counters (zero
-// before the first split call on a workspace; every split call leaves the
-// counters it used zero again), then the zero-point row sums (4 (M + N)
-// bytes), then the split-K partial tiles or the FP6 operand copies; every
-// part 256-byte aligned. A problem that needs no scratch needs no workspace.
+// Caller workspace. Layout: [0, 64 KiB) the split-K and stream-K tile
+// counters (zero before the first such call on a workspace; every call
+// leaves the counters it used zero again), then the zero-point row sums
+// (4 (M + N) bytes), then the split-K partial tiles, or the FP6 operand
+// copies followed by the stream-K partial tiles (either may be absent);
+// every part 256-byte aligned. A problem that needs no scratch needs no
+// workspace.
 constexpr size_t kWsAlign = 256;
 
 size_t align_up(size_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; }
@@ -429,12 +459,23 @@ struct WsPlan {
     size_t sums_off, data_off, total;  // total 0: no workspace needed
 };
 
+// Offset of the stream-K partial tiles in the data part: after the FP6
+// operand copies for the FP6 kernels (which need those copies stream-K or
+// not), at its start for the others.
+size_t sk_partials_off(const Variant &v, int M, int N, int K) {
+    if (v.kind != FP6 && v.kind != FP6WIDE && v.kind != FP6WIDE_SK) return 0;
+    return align_up(F6Geom::bytes(M, K) + F6Geom::bytes(N, K));
+}
+
 WsPlan ws_plan(const Variant &v, int splits, int M, int N, int K, bool zero_points, const SkPlan &sk) {
     const size_t sums = zero_points ? align_up(((size_t)M + N) * 4) : 0;
     size_t data = 0;
-    if (splits > 1) data = (size_t)tile_count(v, M, N) * splits * v.bm * v.bn * 4;
-    else if (sk.on) data = (size_t)(sk.grid - sk.dp_tiles) * v.bm * v.bn * 4;  // one slot per split part
-    else if (v.kind == FP6 || v.kind == FP6WIDE) data = F6Geom::bytes(M, K) + F6Geom::bytes(N, K);
+    if (splits > 1) {
+        data = (size_t)tile_count(v, M, N) * splits * v.bm * v.bn * 4;
+    } else {
+        data = sk_partials_off(v, M, N, K);
+        if (sk.on) data += (size_t)(sk.grid - sk.dp_tiles) * v.bm * v.bn * 4;  // one slot per remainder part
+    }
     if (!sums && !data) return WsPlan{0, 0, 0};
     return WsPlan{kSplitCounterBytes, kSplitCounterBytes + sums, kSplitCounterBytes + sums + data};
 }
@@ -445,9 +486,12 @@ struct Ws {
 };
 
 // INT4 on the FP6 matrix cores fed by the conversion pre-pass: convert both
-// operands into the workspace, then run the FP6 tile kernel.
-hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, const uint8_t *B,
-                      void *C, EpiParams epi, uint8_t *w, hipStream_t stream) {
+// operands into the workspace's data part w, then run the FP6 tile kernel
+// (the stream-K one with its counters and partial tiles: counters, and the
+// data part past the operand copies).
+hipError_t launch_fp6(const Variant &v, const SkPlan &sk, int M, int N, int K, const uint8_t *A,
+                      const uint8_t *B, void *C, EpiParams epi, uint8_t *w, int *counters,
+                      hipStream_t stream) {
     const long Ma = F6Geom::rows_pad(M), Nb = F6Geom::rows_pad(N), runs = F6Geom::runs_pad(K);
     const uint64_t a_bytes = F6Geom::bytes(M, K);
     F6Prep pa{A, w, w + (size_t)Ma * runs * 16, M, (int)Ma, K, (int)runs};
@@ -467,9 +511,20 @@ hipError_t launch_fp6(const Variant &v, int M, int N, int K, const uint8_t *A, c
         // the one-wave-per-SIMD kernel's table entry stores raw sums of whole
         // tiles; ragged or scaled outputs take its shared-epilogue instantiation
         const void *fn = v.fn;
-        if (v.kind == FP6WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) fn = v.fn_epi;
-        void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &epi};
-        e = hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+        if ((v.kind == FP6WIDE || v.kind == FP6WIDE_SK) && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn))
+            fn = v.fn_epi;
+        if (v.kind == FP6WIDE_SK) {
+            SkArgs sa{sk.dp_tiles, sk.parts, nullptr, nullptr};
+            if (sk.on) {
+                sa.counters = counters;
+                sa.partials = reinterpret_cast<uint32_t *>(w + sk_partials_off(v, M, N, K));
+            }
+            void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &sa, &epi};
+            e = hipLaunchKernel(fn, dim3(sk.grid), dim3(v.threads), args, 0, stream);
+        } else {
+            void *args[] = {&ap, &aq, &bp, &bq, &c, &M, &N, &ma, &nb, &kt, &tiles_m, &tiles_n, &epi};
+            e = hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);
+        }
     }
     return e;
 }
@@ -478,7 +533,9 @@ hipError_t launch(int dtype, const Variant &v, int splits, const SkPlan &sk, int
                   const void *B, void *C, EpiParams epi, const WsPlan &plan, Ws ws, hipStream_t stream) {
     const uint8_t *a = static_cast<const uint8_t *>(A);
     const uint8_t *b = static_cast<const uint8_t *>(B);
-    if (v.kind == FP6 || v.kind == FP6WIDE) return launch_fp6(v, M, N, K, a, b, C, epi, ws.p + plan.data_off, stream);
+    if (v.kind == FP6 || v.kind == FP6WIDE || v.kind == FP6WIDE_SK)
+        return launch_fp6(v, sk, M, N, K, a, b, C, epi, ws.p + plan.data_off, reinterpret_cast<int *>(ws.p),
+                          stream);
     if (v.kind == SKINNY) {
         // X = the operand with at most bm rows (A when M is small), W = the other
         int trans = M <= v.bm ? 0 : 1;
@@ -585,8 +642,17 @@ hipError_t choose(int dtype, int variant, int splits, int M, int N, int K, const
         // choice without one
         variant = select_variant(dtype, M, N, K, A, B, C, ws_bytes > 0);
         const Variant &v = t[variant];
-        if (ws_plan(v, 1, M, N, K, zero_points, sk_plan(dtype, v, M, N, K)).total > ws_bytes)
-            variant = select_variant(dtype, M, N, K, A, B, C, false);
+        if (ws_plan(v, 1, M, N, K, zero_points, sk_plan(dtype, v, M, N, K)).total > ws_bytes) {
+            // a stream-K twin whose partial tiles do not fit: its own kernel
+            // with whole tiles where that fits (the FP6 one still needs its
+            // operand copies), else the choice without a workspace
+            const int base = sk_base(variant);
+            const Variant *b = base >= 0 ? &t[base] : nullptr;
+            if (b && ws_plan(*b, 1, M, N, K, zero_points, sk_off(tile_count(*b, M, N))).total <= ws_bytes)
+                variant = base;
+            else
+                variant = select_variant(dtype, M, N, K, A, B, C, false);
+        }
     }
     if (variant >= num_variants(dtype)) return hipErrorInvalidValue;
     const Variant &v = t[variant];

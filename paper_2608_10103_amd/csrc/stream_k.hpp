@@ -1,5 +1,5 @@
 // stream_k.hpp - stream-K schedules of the pipelined and the one-wave-per-SIMD
-// kernels, for problems whose tile count leaves the last round of workgroups
+// kernels (FP16, INT8, and INT4 on the FP6 cores), for problems whose tile count leaves the last round of workgroups
 // partly idle.
 //
 // A problem of T tiles, each KT K-slices deep, is T * KT iterations (one
@@ -34,6 +34,7 @@
 // slots of BM x BN 32-bit words, slot u for remainder workgroup u.
 #pragma once
 
+#include "wide_f6.hpp"
 #include "wide_gemm.hpp"
 
 namespace mpg {
@@ -68,11 +69,12 @@ __device__ __forceinline__ SkWork sk_work(int b, const SkArgs &sk, int KT) {
 // taken from its registers, the others loaded). Slot layout: quad w (values
 // 4w .. 4w + 3) of block (i, j) of thread t in the 16 bytes at vector index
 // ((i FN + j) NQ + w) NT + t, NQ = NV / 4, so each wave's store or load
-// instruction covers 1 KiB. The sum is formed a block row (two with AGPR)
-// at a time, each part's loads of it issued together; this keeps the
-// registers it needs bounded. AGPR: the accumulators live in AGPRs (the
-// one-wave-per-SIMD kernel); each finished block is put back there at once,
-// or the compiler keeps all sums in VGPRs and spills.
+// instruction covers 1 KiB. The sum is formed a few blocks at a time (see
+// below), each part's loads of them
+// issued together; this keeps the registers it needs bounded. AGPR: the
+// accumulators live in AGPRs (the one-wave-per-SIMD kernels); each finished
+// block is put back there at once, or the compiler keeps all sums in VGPRs
+// and spills.
 template <class OutT, int FM, int FN, int NV, int NT, bool AGPR = false, class AccT>
 __device__ __forceinline__ bool sk_fixup(AccT (&acc)[FM][FN], int *counter, uint32_t *slots, int part,
                                          int parts, int *flag) {
@@ -104,48 +106,43 @@ __device__ __forceinline__ bool sk_fixup(AccT (&acc)[FM][FN], int *counter, uint
     }
     __syncthreads();
     if (!flag[0]) return false;
-    // block rows per step: two where the accumulators sit in AGPRs, else one
-    // (the VGPRs hold them too)
-    constexpr int R = (AGPR && FM % 2 == 0) ? 2 : 1;
-    static_assert(FM % R == 0, "whole row pairs");
+    // blocks per step: with the accumulators in AGPRs, two block rows of
+    // 16x16 blocks (64 values per lane) or one 32x32 block (16 values; more
+    // spills); else a block row (the VGPRs hold the accumulators too)
+    constexpr int NB = FM * FN;
+    constexpr int S = AGPR ? (NV >= 16 ? 1 : 64 / NV) : FN;
+    static_assert(NB % S == 0, "whole steps");
 #pragma unroll
-    for (int i0 = 0; i0 < FM; i0 += R) {
-        V sum[R][FN][NQ];
+    for (int b0 = 0; b0 < NB; b0 += S) {
+        V sum[S][NQ];
         for (int q = 0; q < parts; ++q) {
-            V add[R][FN][NQ];
+            V add[S][NQ];
             if (q == part) {
 #pragma unroll
-                for (int r = 0; r < R; ++r)
+                for (int b = 0; b < S; ++b)
 #pragma unroll
-                    for (int j = 0; j < FN; ++j)
-#pragma unroll
-                        for (int w = 0; w < NQ; ++w) add[r][j][w] = quad(acc[i0 + r][j], w);
+                    for (int w = 0; w < NQ; ++w) add[b][w] = quad(acc[(b0 + b) / FN][(b0 + b) % FN], w);
             } else {
                 const V *p = base + (size_t)q * SLOT;
 #pragma unroll
-                for (int r = 0; r < R; ++r)
+                for (int b = 0; b < S; ++b)
 #pragma unroll
-                    for (int j = 0; j < FN; ++j)
-#pragma unroll
-                        for (int w = 0; w < NQ; ++w) add[r][j][w] = p[(((i0 + r) * FN + j) * NQ + w) * NT + tid];
+                    for (int w = 0; w < NQ; ++w) add[b][w] = p[((b0 + b) * NQ + w) * NT + tid];
             }
 #pragma unroll
-            for (int r = 0; r < R; ++r)
+            for (int b = 0; b < S; ++b)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
-#pragma unroll
-                    for (int w = 0; w < NQ; ++w) sum[r][j][w] = q == 0 ? add[r][j][w] : sum[r][j][w] + add[r][j][w];
+                for (int w = 0; w < NQ; ++w) sum[b][w] = q == 0 ? add[b][w] : sum[b][w] + add[b][w];
         }
 #pragma unroll
-        for (int r = 0; r < R; ++r)
+        for (int b = 0; b < S; ++b) {
+            AccT &blk = acc[(b0 + b) / FN][(b0 + b) % FN];
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
+            for (int w = 0; w < NQ; ++w)
 #pragma unroll
-                for (int w = 0; w < NQ; ++w)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) acc[i0 + r][j][4 * w + e] = sum[r][j][w][e];
-                if constexpr (AGPR) asm volatile("" : "+a"(acc[i0 + r][j]));
-            }
+                for (int e = 0; e < 4; ++e) blk[4 * w + e] = sum[b][w][e];
+            if constexpr (AGPR) asm volatile("" : "+a"(blk));
+        }
     }
     if (tid == 0) *counter = 0;  // ready for the next call on this workspace
     return true;
@@ -201,6 +198,32 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm_sk(const uint8
             sk.parts, reinterpret_cast<int *>(lds)))
         return;
     wide_store<DT, PLAIN>(epi, Cv, acc, tm, tn, M, N);
+}
+
+// Stream-K schedule of the one-wave-per-SIMD FP6 kernel (wide_f6_gemm,
+// INT4 on operands converted by the pre-pass): whole 256 x 256 tiles of
+// 128-k slices, grid as for tiled_gemm_sk. The parts add their FP32 sums,
+// integers whose magnitudes add up to at most 64 K < 2^24, so the sum of the
+// parts is exact in any order.
+template <bool PLAIN, int AUX = CP_DEFAULT>
+__global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm_sk(
+    const uint8_t *__restrict__ Ap, const uint8_t *__restrict__ Aq, const uint8_t *__restrict__ Bp,
+    const uint8_t *__restrict__ Bq, int32_t *__restrict__ C, int M, int N, int Ma, int Nb, int KT, int tiles_m,
+    int tiles_n, SkArgs sk, EpiParams epi) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[WideF6Cfg::LDS_BYTES];
+    wf6_entry_args<PLAIN>(C, M, N, epi);
+    const SkWork wk = sk_work(blockIdx.x, sk, KT);
+    int tm, tn;
+    grouped_tile(wk.t, tiles_m, tiles_n, 4, tm, tn);
+    f32x16 acc[4][4];
+    wf6_accumulate<AUX>(lds, Ap, Aq, Bp, Bq, Ma, Nb, KT, tm, tn, wk.k0, wk.len, acc);
+    // flag in the copy buffers, as in tiled_gemm_sk
+    if (wk.u >= 0 &&
+        !sk_fixup<float, 4, 4, 16, WideF6Cfg::NTHREADS, true>(
+            acc, sk.counters + wk.t, sk.partials + (size_t)(wk.u - wk.part) * WideF6Cfg::BM * WideF6Cfg::BN,
+            wk.part, sk.parts, reinterpret_cast<int *>(lds)))
+        return;
+    wf6_store<PLAIN>(epi, C, acc, tm, tn, M, N);
 }
 
 }  // namespace mpg

@@ -63,7 +63,7 @@ typedef F6Cfg<128, 128, 2, 2, 8, 3, 4> F6_128x128_w4_k256_s3;
 
 namespace mpg {
 
-enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5, I4WIDE = 6, TILED_SK = 7, WIDE_SK = 8 };
+enum Kind { GENERIC = 0, TILED = 1, FP6 = 2, SKINNY = 3, WIDE = 4, FP6WIDE = 5, I4WIDE = 6, TILED_SK = 7, WIDE_SK = 8, FP6WIDE_SK = 9 };
 
 struct Variant {
     const char *name;
@@ -74,7 +74,7 @@ struct Variant {
     int threads;
     const void *fn;
     bool splitk;      // kernel takes (splits, counters, partials): the pipelined kernels
-    const void *fn_epi = nullptr;  // WIDE, FP6WIDE, I4WIDE: the instantiation with the
+    const void *fn_epi = nullptr;  // WIDE(_SK), FP6WIDE(_SK), I4WIDE: the instantiation with the
                                    // shared epilogue (ragged edges, scaled outputs); fn
                                    // stores raw sums of whole tiles
 };
@@ -154,9 +154,6 @@ Variant wide(const char *name) {
     return Variant{name, WIDE, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false, fe};
 }
 
-// INT4 on the FP6 cores with the conversion inside the GEMM (wide_i4.hpp);
-// bkb holds the K multiple it needs (in elements). AUX: cache policy of the
-// operand loads.
 // Stream-K schedule of the one-wave-per-SIMD kernel (stream_k.hpp); FP16
 // and INT8 only, like wide().
 template <int DT>
@@ -170,6 +167,9 @@ Variant wide_sk(const char *name) {
     return Variant{name, WIDE_SK, WideCfg::BM, WideCfg::BN, WideCfg::BKB, WideCfg::NTHREADS, f, false, fe};
 }
 
+// INT4 on the FP6 cores with the conversion inside the GEMM (wide_i4.hpp);
+// bkb holds the K multiple it needs (in elements). AUX: cache policy of the
+// operand loads.
 template <int AUX = CP_DEFAULT>
 Variant i4wide(const char *name) {
     kernel_fn k = &wide_i4_gemm<true, AUX>, ke = &wide_i4_gemm<false, AUX>;
@@ -195,6 +195,16 @@ Variant fp6wide(const char *name) {
                           int32_t *, int, int, int, int, int, int, int, EpiParams);
     f6_fn f = &wide_f6_gemm<true, AUX>, fe = &wide_f6_gemm<false, AUX>;
     return Variant{name, FP6WIDE, WideF6Cfg::BM, WideF6Cfg::BN, WideF6Cfg::J, WideF6Cfg::NTHREADS,
+                   reinterpret_cast<const void *>(f), false, reinterpret_cast<const void *>(fe)};
+}
+
+// Stream-K schedule of the one-wave-per-SIMD FP6 kernel (stream_k.hpp).
+template <int AUX = CP_DEFAULT>
+Variant fp6wide_sk(const char *name) {
+    typedef void (*f6sk_fn)(const uint8_t *, const uint8_t *, const uint8_t *, const uint8_t *, int32_t *, int,
+                            int, int, int, int, int, int, SkArgs, EpiParams);
+    f6sk_fn f = &wide_f6_gemm_sk<true, AUX>, fe = &wide_f6_gemm_sk<false, AUX>;
+    return Variant{name, FP6WIDE_SK, WideF6Cfg::BM, WideF6Cfg::BN, WideF6Cfg::J, WideF6Cfg::NTHREADS,
                    reinterpret_cast<const void *>(f), false, reinterpret_cast<const void *>(fe)};
 }
 
@@ -266,7 +276,7 @@ Variant generic(const char *name) {
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
 constexpr int kNumCommon = 57;
-constexpr int kNumFp6 = 16;
+constexpr int kNumFp6 = 17;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 
 // Kernel of the transposed-B entry point (tposeb.hip): F16 or S8, else null.

@@ -23,7 +23,8 @@ const Variant kS4[] = {VARIANT_LIST(S4),
                              i4wide<CP_NT>("e2m3wide256x256_w2x2_k256_nt"),
                              fp6wide<CP_SC0>("fp6wide256x256_w2x2_k128_s3_sc0"),
                              fp6wide<CP_SC1>("fp6wide256x256_w2x2_k128_s3_sc1"),
-                             fp6wide<CP_NT>("fp6wide256x256_w2x2_k128_s3_nt")};
+                             fp6wide<CP_NT>("fp6wide256x256_w2x2_k128_s3_nt"),
+                             fp6wide_sk("fp6wide256x256_w2x2_k128_s3_sk")};
 static_assert(sizeof(kS4) / sizeof(kS4[0]) == kNumS4, "variant count out of date in variants.hpp");
 
 }  // namespace mpg

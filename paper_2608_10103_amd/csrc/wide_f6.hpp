@@ -101,40 +101,34 @@ __device__ __forceinline__ void wf6_chunk(const F6Frag (&a)[4], const F6Frag (&b
     });
 }
 
-// Ap/Aq, Bp/Bq: converted operands; Ma / Nb their padded row counts; KT =
-// padded K / 128 slices (at least 2: K is padded to 256). PLAIN: raw sums to
-// a row-major int32 C of whole 256 x 256 tiles, stored straight from the
-// accumulators; otherwise the shared epilogue (ragged edges, scales). AUX:
-// cache policy of the copy loads.
-template <bool PLAIN, int AUX = CP_DEFAULT>
-__global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
-    const uint8_t *__restrict__ Ap, const uint8_t *__restrict__ Aq, const uint8_t *__restrict__ Bp,
-    const uint8_t *__restrict__ Bq, int32_t *__restrict__ C, int M, int N, int Ma, int Nb, int KT,
-    int tiles_m, int tiles_n, EpiParams epi) {
+// Accumulate slices [kt0, kt0 + KT) of tile (tm, tn) into acc (zeroed
+// here) with the schedule above; KT >= 1 (the prologue's loads of slices
+// kt0 + 1 and kt0 + 2 stay inside the padded workspace or read zeros past
+// it, into buffers no MFMA reads when KT is smaller). Ap/Aq, Bp/Bq: the
+// converted operands, Ma / Nb their padded row counts, KTW the slices of the
+// whole padded K. On return every copy has landed and the accumulators are
+// safe to read; waves may still be reading LDS.
+template <int AUX>
+__device__ __forceinline__ void wf6_accumulate(uint8_t *lds, const uint8_t *Ap, const uint8_t *Aq,
+                                               const uint8_t *Bp, const uint8_t *Bq, int Ma, int Nb, int KTW,
+                                               int tm, int tn, int kt0, int KT, f32x16 (&acc)[4][4]) {
     typedef WideF6Cfg T;
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[T::LDS_BYTES];
-    // the epilogue's arguments are loaded with the others here: a scalar
-    // load still in flight in the loop would make every LDS wait there a
-    // wait for all (scalar loads return out of order)
-    asm volatile("" ::"s"(C), "s"(M), "s"(N));
-    if constexpr (!PLAIN)
-        asm volatile("" ::"s"(epi.scale_a), "s"(epi.scale_b), "s"(epi.zero_a), "s"(epi.zero_b), "s"(epi.sum_a),
-                     "s"(epi.sum_b), "s"(epi.K), "s"(epi.out));
-    const int tid = threadIdx.x, lane = tid & 63;
+    // opaque thread id (see pf_accumulate)
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 31, h = lane >> 5;
     const int wm = wave / 2, wn = wave % 2;
-    int tm, tn;
-    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, 4, tm, tn);
 
-    // run w of slice ks is workspace run 4 ks + w
+    // run w of slice ks is workspace run 4 (kt0 + ks) + w
     WF6Copy c;
-    const int runs = KT * T::J;
+    const int runs = KTW * T::J;
     c.ap = Ap; c.aq = Aq; c.bp = Bp; c.bq = Bq;
     c.apn = runs * Ma * 16; c.aqn = runs * Ma * 8; c.bpn = runs * Nb * 16; c.bqn = runs * Nb * 8;
-    c.ap0 = (wave * Ma + tm * T::BM) * 16; c.aq0 = (wave * Ma + tm * T::BM) * 8;
-    c.bp0 = (wave * Nb + tn * T::BN) * 16; c.bq0 = (wave * Nb + tn * T::BN) * 8;
     c.aps = T::J * Ma * 16; c.aqs = T::J * Ma * 8; c.bps = T::J * Nb * 16; c.bqs = T::J * Nb * 8;
+    c.ap0 = (wave * Ma + tm * T::BM) * 16 + kt0 * c.aps; c.aq0 = (wave * Ma + tm * T::BM) * 8 + kt0 * c.aqs;
+    c.bp0 = (wave * Nb + tn * T::BN) * 16 + kt0 * c.bps; c.bq0 = (wave * Nb + tn * T::BN) * 8 + kt0 * c.bqs;
     c.voff = (uint32_t)lane * 16;
     // stage image: each part holds runs 0..3 of 256 rows, run w at
     // w * 256 * 16 (P) or w * 256 * 8 (Q) from the part's start
@@ -147,7 +141,6 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
     const int pb0 = T::BP + rowb * 16, qb0 = T::BQ + rowb * 8;
     constexpr int KCP = 2 * T::BM * 16, KCQ = 2 * T::BM * 8;  // next k-chunk: two runs on
 
-    f32x16 acc[4][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -200,7 +193,18 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j) asm volatile("" : "+a"(acc[i][j]));
+}
 
+// Accumulators of a finished tile to C: PLAIN, raw sums of a whole tile
+// stored straight from the accumulators; otherwise the shared epilogue
+// (ragged edges, scales).
+template <bool PLAIN>
+__device__ __forceinline__ void wf6_store(const EpiParams &epi, int32_t *C, const f32x16 (&acc)[4][4], int tm,
+                                          int tn, int M, int N) {
+    typedef WideF6Cfg T;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 31, h = lane >> 5;
+    const int wm = wave / 2, wn = wave % 2;
     const long row0 = (long)tm * T::BM + wm * 128;
     const long col0 = (long)tn * T::BN + wn * 128 + r;
     if constexpr (PLAIN) {
@@ -218,6 +222,37 @@ __global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
     } else {
         epi_store_tile<S4, 32, 4, 4, 16>(epi, C, acc, row0, col0, h, M, N, ConvToInt());
     }
+}
+
+// Consume the kernel arguments the epilogue reads (C, M, N and the epilogue
+// parameters) at entry: a scalar load of them still in flight in the loop
+// would make every LDS wait there a wait for all (scalar loads return out of
+// order).
+template <bool PLAIN>
+__device__ __forceinline__ void wf6_entry_args(const int32_t *C, int M, int N, const EpiParams &epi) {
+    asm volatile("" ::"s"(C), "s"(M), "s"(N));
+    if constexpr (!PLAIN)
+        asm volatile("" ::"s"(epi.scale_a), "s"(epi.scale_b), "s"(epi.zero_a), "s"(epi.zero_b), "s"(epi.sum_a),
+                     "s"(epi.sum_b), "s"(epi.K), "s"(epi.out));
+}
+
+// Ap/Aq, Bp/Bq: converted operands; Ma / Nb their padded row counts; KT =
+// padded K / 128 slices (at least 2: K is padded to 256). PLAIN: raw sums to
+// a row-major int32 C of whole 256 x 256 tiles, stored straight from the
+// accumulators; otherwise the shared epilogue (ragged edges, scales). AUX:
+// cache policy of the copy loads.
+template <bool PLAIN, int AUX = CP_DEFAULT>
+__global__ __launch_bounds__(WideF6Cfg::NTHREADS, 1) void wide_f6_gemm(
+    const uint8_t *__restrict__ Ap, const uint8_t *__restrict__ Aq, const uint8_t *__restrict__ Bp,
+    const uint8_t *__restrict__ Bq, int32_t *__restrict__ C, int M, int N, int Ma, int Nb, int KT,
+    int tiles_m, int tiles_n, EpiParams epi) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[WideF6Cfg::LDS_BYTES];
+    wf6_entry_args<PLAIN>(C, M, N, epi);
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, 4, tm, tn);
+    f32x16 acc[4][4];
+    wf6_accumulate<AUX>(lds, Ap, Aq, Bp, Bq, Ma, Nb, KT, tm, tn, 0, KT, acc);
+    wf6_store<PLAIN>(epi, C, acc, tm, tn, M, N);
 }
 
 }  // namespace mpg

@@ -647,6 +647,7 @@ def _named(dtype, name):
 
 SK_WIDE, SK_PIPE, SK_SPREAD = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk",
                                "spread128x128_w2x2_k128_s4_sk")
+SK_F6 = "fp6wide256x256_w2x2_k128_s3_sk"  # INT4 on the FP6 cores, converted operands
 # tile counts just past one or two rounds of 256 workgroups (one per CU),
 # K deep enough for the schedule to split the remaining tiles
 SK_CASES = [
@@ -661,6 +662,10 @@ SK_CASES = [
     ("s8", SK_SPREAD, 128 * 16 + 5, 128 * 16, 8192),
     ("s4", SK_SPREAD, 2100, 2000, 12800),
     ("s4", SK_SPREAD, 128 * 23 + 5, 128 * 12, 16384),
+    ("s4", SK_F6, 4352, 4096, 16384),      # 272 tiles: 16 in 4 parts of 32 slices
+    ("s4", SK_F6, 6144, 6400, 32768),      # 600 tiles: 88 in 2 parts
+    ("s4", SK_F6, 4000, 4400, 32768),      # ragged edges (shared epilogue), 288 tiles
+    ("s4", SK_F6, 1000, 700, 30000),       # 12 tiles, all split; K padded to 30208
 ]
 
 
@@ -682,7 +687,13 @@ def test_stream_k_parity(dtype, name, M, N, K):
     C = mp.GEMM[dtype](Ad, Bd, variant=v, workspace=ws)
     for _ in range(3):
         assert torch.equal(C, mp.GEMM[dtype](Ad, Bd, variant=v, workspace=ws))
-    whole = mp.GEMM[dtype](Ad, Bd, variant=v)
+    # whole tiles: no room for partial tiles (the FP6 kernel still needs its
+    # converted operands: a workspace of the whole-tile kernel's size)
+    whole_ws = None
+    if name == SK_F6:
+        base = _named(dtype, name[:-3])
+        whole_ws = mp.new_workspace(mp.workspace_size(dtype, M, N, K, variant=base, splits=1), "cuda")
+    whole = mp.GEMM[dtype](Ad, Bd, variant=v, workspace=whole_ws)
     torch.cuda.synchronize()
     assert int(ws[:65536].count_nonzero()) == 0, "counters left non-zero"
     rows = np.array(sorted(set(range(0, M, 13)) | {M - 1}))
@@ -697,10 +708,13 @@ def test_stream_k_parity(dtype, name, M, N, K):
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_stream_k_scaled(dtype):
     """The scaled epilogue (and zero points for integers) through stream-K
-    on the one-wave-per-SIMD kernel (FP16, INT8) and the 128 x 128 one."""
+    on the one-wave-per-SIMD kernels (FP16, INT8; INT4 on the FP6 cores) and
+    the 128 x 128 one."""
     cases = [(SK_SPREAD, 2100, 2000, {"f16": 3200, "s8": 6400, "s4": 12800}[dtype])]
     if dtype != "s4":
         cases.append((SK_WIDE, 2048, 2048, {"f16": 4096, "s8": 8192}[dtype]))
+    else:
+        cases.append((SK_F6, 500, 700, 30000))  # 6 tiles in 5 parts, ragged
     for i, (name, M, N, K) in enumerate(cases):
         v = _named(dtype, name)
         assert mp.sk_schedule(dtype, v, M, N, K)[1] > 1
@@ -712,6 +726,23 @@ def test_stream_k_scaled(dtype):
         C = _run_scaled(dtype, A, B, out, sa, sb, za, zb, variant=v)
         _, exact, D = oracle.gemm_scaled(dtype, A, B, out, sa, sb, za, zb)
         assert_scaled(C, exact, D, out, f"stream-K {dtype} {name} {M}x{N}x{K} {out} zp={zp}")
+
+
+@pytest.mark.parametrize("dtype,K", [("f16", 8192), ("s8", 16384), ("s4", 16384)])
+def test_stream_k_through_the_entry_point(dtype, K):
+    """272 tiles of 256 x 256 with a workspace sized by the library for its
+    own choice: the entry point takes the stream-K twin of its whole-tile
+    kernel (INT4: the FP6 pre-pass one) and matches the oracle on sampled
+    rows."""
+    M, N = 4352, 4096
+    v = mp.select_variant(dtype, M, N, K, with_ws=True)
+    assert mp.variant_name(dtype, v).endswith("_sk") and mp.sk_schedule(dtype, v, M, N, K)[1] > 1
+    _log(f"stream-K entry point {dtype} {M}x{N}x{K}: {mp.variant_name(dtype, v)}")
+    A, B = si.gen_operands(dtype, M, N, K, seed=K + 7)
+    C = mp.GEMM[dtype](dev(A), dev(B), workspace="auto")
+    rows = np.array([0, 1, 255, 256, 2047, 4095, 4096, 4351])
+    assert_parity(dtype, C.cpu().numpy()[rows], *oracle_gemm(dtype, A, B, rows=rows),
+                  f"stream-K entry point {dtype} {M}x{N}x{K}")
 
 
 # ---------------------------------------------------------------- scaled outputs (fused epilogue)

@@ -13,7 +13,8 @@ import pytest
 import paper_2608_10103_amd as mp
 
 G = 256
-SK_NAMES = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk", "spread128x128_w2x2_k128_s4_sk")
+SK_NAMES = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk", "spread128x128_w2x2_k128_s4_sk",
+            "fp6wide256x256_w2x2_k128_s3_sk")
 BYTES_PER_ELEM = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 
 
@@ -22,7 +23,23 @@ def _variant(dtype, name):
 
 
 def _tile(name):
-    return tuple(int(x) for x in re.match(r"[a-z]+(\d+)x(\d+)_", name).groups())
+    return tuple(int(x) for x in re.search(r"(\d+)x(\d+)_w", name).groups())
+
+
+def _slices(dtype, name, K):
+    """K-slices per tile: 128-byte slices of a row; the FP6 kernel's 128-k
+    slices of K padded to 256 (its converted operands' padding)."""
+    if name.startswith("fp6"):
+        return -(-K // 256) * 2
+    return int(K * BYTES_PER_ELEM[dtype]) // 128
+
+
+def _f6_bytes(M, N, K):
+    """The FP6 operand copies the INT4 pre-pass writes (24 bytes per row and
+    run of 32 k, rows padded to 256, K to 256), 256-byte aligned."""
+    runs = -(-K // 256) * 8
+    b = (-(-M // 256) * 256 + -(-N // 256) * 256) * runs * 24
+    return -(-b // 256) * 256
 
 
 def _work(b, dp, parts, KT):
@@ -50,6 +67,13 @@ CASES = [  # dtype, name, M, N, K
     ("s8", SK_NAMES[2], 2100, 2000, 8192),       # 272 tiles of 128 x 128
     ("s4", SK_NAMES[2], 128 * 23 + 5, 128 * 12, 32768),
     ("f16", SK_NAMES[2], 128 * 16 + 1, 128 * 16, 128 * 3),  # 3 slices: off
+    ("s4", SK_NAMES[3], 4352, 4096, 16384),      # INT4 on the FP6 cores: 128 slices of 128 k
+    ("s4", SK_NAMES[3], 4000, 4400, 12800),      # ragged: 288 tiles, 100 slices: off
+    ("s4", SK_NAMES[3], 4000, 4400, 32768),      # 256 slices: on
+    ("s4", SK_NAMES[3], 4352, 4096, 30000),      # K padded to 30208: 236 slices
+    ("s4", SK_NAMES[3], 4352, 4096, 8192),       # 64 slices: off
+    ("s4", SK_NAMES[3], 256 * 3, 256 * 86, 81920),  # 258 tiles, 640 slices: 8 parts
+    ("s4", SK_NAMES[3], 33, 65, 1 << 18),        # one tile
 ]
 
 
@@ -58,14 +82,16 @@ def test_sk_schedule_covers_every_iteration_once(dtype, name, M, N, K):
     v = _variant(dtype, name)
     bm, bn = _tile(name)
     tiles = -(-M // bm) * -(-N // bn)
-    KT = int(K * BYTES_PER_ELEM[dtype]) // 128
+    KT = _slices(dtype, name, K)
     dp, parts, grid = mp.sk_schedule(dtype, v, M, N, K)
     q, r = divmod(tiles, G)
-    # the library's cost model: s = round(sqrt(KT / 5)) capped at G / r and
-    # 8, taken when KT (1 - 1/s) - 5 (s - 1) - 13 exceeds KT / 10
-    want_parts = min(int(math.sqrt(KT / 5) + 0.5), G // r, 8) if r and 2 * r <= G else 1
-    gain = KT * (1 - 1 / want_parts) - 5 * (want_parts - 1) - 13 if want_parts >= 2 else 0
-    if want_parts < 2 or gain <= KT / 10:
+    # the library's cost model (slice time t, margin m: 1 and 0.1, for the
+    # FP6 kernel 0.5 and 0.25): s = round(sqrt(KT t / 5)) capped at G / r, 8
+    # and KT / 2, taken when KT t (1 - 1/s) - 5 (s - 1) - 13 exceeds m KT t
+    t, m = (0.5, 0.25) if name.startswith("fp6") else (1.0, 0.1)
+    want_parts = min(int(math.sqrt(KT * t / 5) + 0.5), G // r, 8, KT // 2) if r and 2 * r <= G else 1
+    gain = KT * t * (1 - 1 / want_parts) - 5 * (want_parts - 1) - 13 if want_parts >= 2 else 0
+    if want_parts < 2 or gain <= m * KT * t:
         assert (dp, parts, grid) == (tiles, 1, tiles)
         return
     assert (dp, parts, grid) == (q * G, want_parts, q * G + r * want_parts)
@@ -86,7 +112,9 @@ def test_sk_schedule_covers_every_iteration_once(dtype, name, M, N, K):
         assert all(a[0] + a[1] == b[0] for a, b in zip(sorted(ps), sorted(ps)[1:])), f"tile {t} parts not contiguous"
         assert sum(n for _, n in ps) == KT
     assert slots == set(range(grid - dp))
-    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == 65536 + (grid - dp) * bm * bn * 4
+    # counters, then (FP6 kernel) the converted operands, then one partial slot per remainder part
+    f6 = _f6_bytes(M, N, K) if name.startswith("fp6") else 0
+    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == 65536 + f6 + (grid - dp) * bm * bn * 4
 
 
 @pytest.mark.parametrize("dtype,name,M,N,K", [
@@ -96,6 +124,7 @@ def test_sk_schedule_covers_every_iteration_once(dtype, name, M, N, K):
     ("s8", SK_NAMES[0], 256 * 20, 256 * 20, 1024),  # 400 = 256 + 144: last round over half full
     ("s4", SK_NAMES[2], 2048, 2048, 512),         # 256 tiles
     ("s8", "pipe256x256_w2x4_k128_s2", 4352, 4096, 1024),  # not a stream-K variant
+    ("s4", SK_NAMES[3], 8192, 8192, 8192),        # 1024 tiles: whole rounds
 ])
 def test_sk_schedule_off(dtype, name, M, N, K):
     """Whole rounds, a last round over half full, or a variant without the
@@ -104,7 +133,9 @@ def test_sk_schedule_off(dtype, name, M, N, K):
     bm, bn = _tile(name)
     tiles = -(-M // bm) * -(-N // bn)
     assert mp.sk_schedule(dtype, v, M, N, K) == (tiles, 1, tiles)
-    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == 0
+    # no scratch but the FP6 kernel's converted operands
+    f6 = 65536 + _f6_bytes(M, N, K) if name.startswith("fp6") else 0
+    assert mp.workspace_size(dtype, M, N, K, variant=v, splits=1) == f6
 
 
 def test_sk_schedule_errors():
@@ -118,6 +149,11 @@ def test_sk_schedule_errors():
     # the one-wave-per-SIMD kernel needs whole tiles; it has no INT4 kernel
     assert L.mpgemm_sk_schedule(0, v, 4353, 4096, 512, p, p, p) == 1
     assert L.mpgemm_sk_schedule(2, _variant("s4", SK_NAMES[0]), 4352, 4096, 512, p, p, p) == 1
+    # the FP6 kernel: INT4 only, even K
+    f6 = _variant("s4", SK_NAMES[3])
+    assert L.mpgemm_sk_schedule(0, f6, 4352, 4096, 512, p, p, p) == 1
+    assert L.mpgemm_sk_schedule(2, f6, 4352, 4096, 511, p, p, p) == 1
+    assert L.mpgemm_sk_schedule(2, f6, 4352, 4096, 512, p, p, p) == 0
 
 
 def test_sk_selection_with_a_workspace():
@@ -137,5 +173,7 @@ def test_sk_selection_with_a_workspace():
     # schedule off: too few slices, whole rounds, last round over half full
     for d, M, N, K in [("s8", 4352, 4096, 4096), ("f16", 8192, 8192, 8192), ("f16", 5120, 5120, 8192)]:
         assert not name(d, M, N, K, True).endswith("_sk"), (d, M, N, K)
-    # INT4 with a workspace keeps the FP6 pre-pass kernel (no stream-K twin)
-    assert name("s4", 4352, 4096, 16384, True) == "fp6wide256x256_w2x2_k128_s3"
+    # INT4 with a workspace: the FP6 pre-pass kernel, stream-K where its plan is on
+    assert name("s4", 4352, 4096, 16384, True) == "fp6wide256x256_w2x2_k128_s3_sk"
+    assert name("s4", 8192, 8192, 8192, True) == "fp6wide256x256_w2x2_k128_s3"
+    assert name("s4", 4352, 4096, 16384, False) == "e2m3wide256x256_w2x2_k256"
