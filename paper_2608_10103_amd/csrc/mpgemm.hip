@@ -173,9 +173,10 @@ int resident_groups() {
 //
 // Cost model, in microseconds (timelines of the kernels at 4352 x 4096 x
 // {4096, 8192} on MI355X): a remainder tile's time without stream-K is
-// KT t (KT K-slices of t each: t about 1 us for a 256 x 256 tile, FP16 and
-// INT8 alike, proportionally less for 128 x 128 tiles, whose partials are
-// proportionally smaller; about 0.5 us for the FP6 kernel's 128-k slices);
+// KT t (KT K-slices of t each: t about 1 us for a 128-byte slice of a
+// 256 x 256 tile, FP16 and INT8 alike, proportionally less for 128 x 128
+// tiles, whose partials are proportionally smaller, so t = 1 for them too;
+// half for 64-byte slices; about 0.5 us for the FP6 kernel's 128-k slices);
 // with s parts it is KT t / s, plus about 5 per partial tile the finishing
 // part loads (s - 1; one workgroup reads them at about 50 GB/s) and about
 // 13 for publishing, fencing and counting. Gain(s) = KT t (1 - 1/s) -
@@ -201,12 +202,16 @@ SkPlan sk_plan(int dtype, const Variant &v, int M, int N, int K) {
     if (!is_sk(v) || tiles > kSplitCounters) return sk_off(tiles);
     const long G = resident_groups(), r = tiles % G;
     if (r == 0 || 2 * r > G) return sk_off(tiles);
+    // 128 x 128 tiles with no whole round before the remainder: splitting the
+    // few tiles measured slower (FP16 1200 x 1100 x 4096, 90 tiles in 2 parts:
+    // 31.3 against 28.8 us)
+    if (tiles < G && (long)v.bm * v.bn < 256 * 256) return sk_off(tiles);
     // slices per tile (the FP6 kernel: 128-k slices of the padded K), the
     // time of a lone remainder tile's slice in microseconds, and the margin
     // the modelled gain must clear (a fraction of the remainder round)
     const bool f6 = v.kind == FP6WIDE_SK;
     const long KT = f6 ? F6Geom::runs_pad(K) / v.bkb : row_bytes(dtype, K) / v.bkb;
-    const double t = f6 ? 0.5 : 1.0, margin = f6 ? 0.25 : 0.1;
+    const double t = f6 ? 0.5 : v.bkb / 128.0, margin = f6 ? 0.25 : 0.1;
     long parts = (long)(sqrt(KT * t / 5.0) + 0.5);
     if (parts > G / r) parts = G / r;
     if (parts > kSkMaxParts) parts = kSkMaxParts;
@@ -257,6 +262,8 @@ int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
 enum : int {
     V_PIPE256_W2X4 = 9,      // pipe256x256_w2x4_k128_s2
     V_WIDE = 50,             // wide256x256_w2x2_k128_m16
+    V_SPREAD128W8 = 54,      // spread128x128_w2x4_k128_s4
+    V_SPREAD128W8_K64 = 55,  // spread128x128_w2x4_k64_s4
     V_SPREAD128_K128 = 20,   // spread128x128_w2x2_k128_s4
     V_SPREAD128_K64 = 21,    // spread128x128_w2x2_k64_s4
     V_STAGED256_W2X4 = 25,   // staged256x256_w2x4_k128_n1
@@ -264,9 +271,10 @@ enum : int {
     V_SKINNY = 38,           // skinny16x16_k64; then 16x32, 32x16, 32x32
     V_SKINNY16_D8 = 42,      // skinny16x32_k64_d8
 };
-// The stream-K schedules of three of them, the last entries of the common
+// The stream-K schedules of five of them, the last entries of the common
 // list.
-constexpr int V_WIDE_SK = kNumCommon - 3, V_PIPE256_SK = kNumCommon - 2, V_SPREAD128_SK = kNumCommon - 1;
+constexpr int V_WIDE_SK = kNumCommon - 5, V_PIPE256_SK = kNumCommon - 4, V_SPREAD128_SK = kNumCommon - 3,
+              V_SPREAD128W8_SK = kNumCommon - 2, V_SPREAD128W8_K64_SK = kNumCommon - 1;
 
 // INT4-only variants follow the common list in kS4.
 constexpr int V_FP6_256_S2 = kNumCommon + 1;  // fp6pipe256x256_w2x4_k128_s2
@@ -282,6 +290,8 @@ int sk_twin(int variant) {
         case V_WIDE: return V_WIDE_SK;
         case V_PIPE256_W2X4: return V_PIPE256_SK;
         case V_SPREAD128_K128: return V_SPREAD128_SK;
+        case V_SPREAD128W8: return V_SPREAD128W8_SK;
+        case V_SPREAD128W8_K64: return V_SPREAD128W8_K64_SK;
         case V_FP6_WIDE: return V_FP6_WIDE_SK;
         default: return -1;
     }
@@ -293,6 +303,8 @@ int sk_base(int variant) {
         case V_WIDE_SK: return V_WIDE;
         case V_PIPE256_SK: return V_PIPE256_W2X4;
         case V_SPREAD128_SK: return V_SPREAD128_K128;
+        case V_SPREAD128W8_SK: return V_SPREAD128W8;
+        case V_SPREAD128W8_K64_SK: return V_SPREAD128W8_K64;
         case V_FP6_WIDE_SK: return V_FP6_WIDE;
         default: return -1;
     }
@@ -315,20 +327,27 @@ struct Pref { int variant; long min_tiles; };
 // for the in-GEMM conversion, whose 16-half-line register loads and
 // conversion do not overlap the MFMAs), then the 8-wave one where the first's
 // 32-bit workspace offsets do not reach.
-// FP16, INT8: below 256 tiles of 256 x 256 the 128-byte-slice 128 x 128
-// kernel (as fast or faster than the 64-byte one at every measured size:
-// square N = 512 ... 2048 and M = 256 x 8192 x 8192), the 64-byte one when
-// K does not fill 128-byte slices.
+// FP16, INT8: below 256 tiles of 256 x 256 the 128 x 128 kernel with eight
+// waves of 64 x 32 and 128-byte slices, the 64-byte one when K does not fill
+// 128-byte slices. Against the four-wave 128 x 128 kernel (64 x 64 waves)
+// chosen before, interleaved on MI355X at 512^3 ... 2560^3, 1024 x 8192 x
+// 2048, 2048 x 4096 x 1024, 2000 x 1900 x 2048, 1000 x 3000 x 4096,
+// 3968^2 x 4096 and 2100 x 2000 x 6400: FP16 1.06-1.32x, INT8 1.10-1.43x
+// faster (more waves keep more copies and MFMAs in flight per CU).
+// INT4 (no FP6 kernel): the eight-wave kernel with 64-byte slices (128 k),
+// 1.11-1.37x faster than the four-wave 128-byte-slice kernel at the same
+// shapes.
 // FP16, INT8: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles
 // fill the CUs (1.09-1.21x the 8-wave kernel for FP16, 1.12-1.23x for INT8,
 // at 2048..16384 x 4096..16384 x 2048..16384); the 8-wave kernel, with
 // predicated edges, where M or N is not a multiple of 256.
-const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128_K128, 1}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_I4WIDE, 256}, {V_STAGED256_W2X4, 256}, {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1},
+const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
+                         {V_PIPE64, 1}};
+const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                         {V_PIPE64, 1}};
+const Pref kPrefS4[] = {{V_I4WIDE, 256}, {V_STAGED256_W2X4, 256}, {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 256}, {V_FP6_256_S2, 512}, {V_I4WIDE, 256}, {V_STAGED256_W2X4, 256},
-                          {V_SPREAD128_K128, 256}, {V_SPREAD128_K64, 1}, {V_PIPE64, 1}};
+                          {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the
 // narrow tiles below (measured on MI355X at 1..32 x {4096, 8192, 14336,

@@ -37,6 +37,9 @@ typedef TileCfg<256, 256, 2, 2, 64, 4, 4> T256x256_w4_k64_s4;
 typedef TileCfg<256, 128, 2, 2, 128, 3, 4> T256x128_w4_s3;
 typedef TileCfg<128, 128, 2, 2, 128, 2, 4> T128x128_w4_s2;
 typedef TileCfg<128, 128, 2, 2, 128, 4, 4> T128x128_w4_s4;
+// eight waves of 64 x 32 on a 128 x 128 tile (mid sizes)
+typedef TileCfg<128, 128, 2, 4, 128, 4, 4> T128x128_w8_s4;
+typedef TileCfg<128, 128, 2, 4, 64, 4, 4> T128x128_w8_k64_s4;
 typedef TileCfg<64, 64, 1, 1, 128, 4, 4> T64x64_w1_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 4, 4> T256x256_w8_k64_s4;
 typedef TileCfg<256, 256, 2, 4, 64, 3, 4> T256x256_w8_k64_s3;
@@ -269,13 +272,17 @@ Variant generic(const char *name) {
      wide<DT, CP_SC0>("wide256x256_w2x2_k128_m16_sc0"),                    \
      wide<DT, CP_SC1>("wide256x256_w2x2_k128_m16_sc1"),                    \
      wide<DT, CP_NT>("wide256x256_w2x2_k128_m16_nt"),                     \
+     pipelined<DT, T128x128_w8_s4, true>("spread128x128_w2x4_k128_s4"),    \
+     pipelined<DT, T128x128_w8_k64_s4, true>("spread128x128_w2x4_k64_s4"), \
      wide_sk<DT>("wide256x256_w2x2_k128_m16_sk"),                          \
      pipelined_sk<DT, T256x256_w8_s2, false>("pipe256x256_w2x4_k128_s2_sk"), \
-     pipelined_sk<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4_sk")
+     pipelined_sk<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4_sk"), \
+     pipelined_sk<DT, T128x128_w8_s4, true>("spread128x128_w2x4_k128_s4_sk"), \
+     pipelined_sk<DT, T128x128_w8_k64_s4, true>("spread128x128_w2x4_k64_s4_sk")
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 57;
+constexpr int kNumCommon = 61;
 constexpr int kNumFp6 = 17;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -123,9 +123,9 @@ def test_selection_at_sweep_sizes():
     want = {
         8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
-        2048: ("spread128x128_w2x2_k128_s4",) * 3,
-        1024: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
-        512: ("spread128x128_w2x2_k128_s4",) * 2 + ("spread128x128_w2x2_k64_s4",),
+        2048: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
+        1024: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
+        512: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
     }
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))

@@ -648,6 +648,7 @@ def _named(dtype, name):
 SK_WIDE, SK_PIPE, SK_SPREAD = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk",
                                "spread128x128_w2x2_k128_s4_sk")
 SK_F6 = "fp6wide256x256_w2x2_k128_s3_sk"  # INT4 on the FP6 cores, converted operands
+SK_W8, SK_W8K64 = "spread128x128_w2x4_k128_s4_sk", "spread128x128_w2x4_k64_s4_sk"  # eight waves of 64 x 32
 # tile counts just past one or two rounds of 256 workgroups (one per CU),
 # K deep enough for the schedule to split the remaining tiles
 SK_CASES = [
@@ -666,10 +667,14 @@ SK_CASES = [
     ("s4", SK_F6, 6144, 6400, 32768),      # 600 tiles: 88 in 2 parts
     ("s4", SK_F6, 4000, 4400, 32768),      # ragged edges (shared epilogue), 288 tiles
     ("s4", SK_F6, 1000, 700, 30000),       # 12 tiles, all split; K padded to 30208
+    ("f16", SK_W8, 2100, 2000, 3200),      # 272 tiles of 128 x 128, 3 parts
+    ("s8", SK_W8, 2100, 2000, 8192),
+    ("s4", SK_W8K64, 2100, 2000, 12800),   # 64-byte slices
+    ("s4", SK_W8K64, 128 * 23 + 5, 128 * 12, 16384),
 ]
 
 
-@pytest.mark.parametrize("dtype,name,M,N,K", SK_CASES, ids=[f"{c[0]}-{c[1][:6]}-{c[2]}x{c[3]}x{c[4]}" for c in SK_CASES])
+@pytest.mark.parametrize("dtype,name,M,N,K", SK_CASES, ids=[f"{c[0]}-{c[1][:-3]}-{c[2]}x{c[3]}x{c[4]}" for c in SK_CASES])
 def test_stream_k_parity(dtype, name, M, N, K):
     """Stream-K variants where their schedule splits tiles into K-parts:
     every 13th row (and the last) against the oracle (bit-exact integers,
@@ -710,7 +715,8 @@ def test_stream_k_scaled(dtype):
     """The scaled epilogue (and zero points for integers) through stream-K
     on the one-wave-per-SIMD kernels (FP16, INT8; INT4 on the FP6 cores) and
     the 128 x 128 one."""
-    cases = [(SK_SPREAD, 2100, 2000, {"f16": 3200, "s8": 6400, "s4": 12800}[dtype])]
+    cases = [(SK_SPREAD, 2100, 2000, {"f16": 3200, "s8": 6400, "s4": 12800}[dtype]),
+             (SK_W8K64 if dtype == "s4" else SK_W8, 2100, 2000, {"f16": 3200, "s8": 6400, "s4": 12800}[dtype])]
     if dtype != "s4":
         cases.append((SK_WIDE, 2048, 2048, {"f16": 4096, "s8": 8192}[dtype]))
     else:

@@ -14,7 +14,7 @@ import paper_2608_10103_amd as mp
 
 G = 256
 SK_NAMES = ("wide256x256_w2x2_k128_m16_sk", "pipe256x256_w2x4_k128_s2_sk", "spread128x128_w2x2_k128_s4_sk",
-            "fp6wide256x256_w2x2_k128_s3_sk")
+            "fp6wide256x256_w2x2_k128_s3_sk", "spread128x128_w2x4_k128_s4_sk", "spread128x128_w2x4_k64_s4_sk")
 BYTES_PER_ELEM = {"f16": 2.0, "s8": 1.0, "s4": 0.5}
 
 
@@ -31,7 +31,7 @@ def _slices(dtype, name, K):
     slices of K padded to 256 (its converted operands' padding)."""
     if name.startswith("fp6"):
         return -(-K // 256) * 2
-    return int(K * BYTES_PER_ELEM[dtype]) // 128
+    return int(K * BYTES_PER_ELEM[dtype]) // (64 if "_k64_" in name else 128)
 
 
 def _f6_bytes(M, N, K):
@@ -74,6 +74,10 @@ CASES = [  # dtype, name, M, N, K
     ("s4", SK_NAMES[3], 4352, 4096, 8192),       # 64 slices: off
     ("s4", SK_NAMES[3], 256 * 3, 256 * 86, 81920),  # 258 tiles, 640 slices: 8 parts
     ("s4", SK_NAMES[3], 33, 65, 1 << 18),        # one tile
+    ("s8", SK_NAMES[4], 2100, 2000, 8192),       # eight-wave 128 x 128 kernel
+    ("f16", SK_NAMES[4], 2100, 2000, 3200),
+    ("s4", SK_NAMES[5], 2100, 2000, 12800),      # 64-byte slices: 100 slices of half the time
+    ("s4", SK_NAMES[5], 128 * 23 + 5, 128 * 12, 32768),
 ]
 
 
@@ -85,11 +89,14 @@ def test_sk_schedule_covers_every_iteration_once(dtype, name, M, N, K):
     KT = _slices(dtype, name, K)
     dp, parts, grid = mp.sk_schedule(dtype, v, M, N, K)
     q, r = divmod(tiles, G)
-    # the library's cost model (slice time t, margin m: 1 and 0.1, for the
-    # FP6 kernel 0.5 and 0.25): s = round(sqrt(KT t / 5)) capped at G / r, 8
-    # and KT / 2, taken when KT t (1 - 1/s) - 5 (s - 1) - 13 exceeds m KT t
-    t, m = (0.5, 0.25) if name.startswith("fp6") else (1.0, 0.1)
-    want_parts = min(int(math.sqrt(KT * t / 5) + 0.5), G // r, 8, KT // 2) if r and 2 * r <= G else 1
+    # the library's cost model (slice time t, margin m: 1 and 0.1, 0.5 for
+    # 64-byte slices, for the FP6 kernel 0.5 and 0.25): s = round(sqrt(KT t
+    # / 5)) capped at G / r, 8 and KT / 2, taken when KT t (1 - 1/s) -
+    # 5 (s - 1) - 13 exceeds m KT t
+    t, m = (0.5, 0.25) if name.startswith("fp6") else ((0.5 if "_k64_" in name else 1.0), 0.1)
+    small_tile_first_round = tiles < G and bm * bn < 256 * 256  # 128 x 128 tiles need a whole round first
+    want_parts = (min(int(math.sqrt(KT * t / 5) + 0.5), G // r, 8, KT // 2)
+                  if r and 2 * r <= G and not small_tile_first_round else 1)
     gain = KT * t * (1 - 1 / want_parts) - 5 * (want_parts - 1) - 13 if want_parts >= 2 else 0
     if want_parts < 2 or gain <= m * KT * t:
         assert (dp, parts, grid) == (tiles, 1, tiles)
@@ -165,8 +172,9 @@ def test_sk_selection_with_a_workspace():
         ("f16", 4352, 4096, 8192, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
         ("s8", 4352, 4096, 16384, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
         ("f16", 4000, 4400, 6400, "pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2_sk"),
-        ("s8", 2100, 2000, 6400, "spread128x128_w2x2_k128_s4", "spread128x128_w2x2_k128_s4_sk"),
-        ("s4", 2100, 2000, 12800, "spread128x128_w2x2_k128_s4", "spread128x128_w2x2_k128_s4_sk"),
+        ("s8", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
+        ("s4", 2100, 2000, 12800, "spread128x128_w2x4_k64_s4", "spread128x128_w2x4_k64_s4_sk"),
+        ("f16", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
     ]:
         assert name(d, M, N, K, False) == plain, (d, M, N, K)
         assert name(d, M, N, K, True) == twin, (d, M, N, K)
