@@ -340,13 +340,21 @@ struct Pref { int variant; long min_tiles; };
 // FP16, INT8: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles
 // fill the CUs (1.09-1.21x the 8-wave kernel for FP16, 1.12-1.23x for INT8,
 // at 2048..16384 x 4096..16384 x 2048..16384); the 8-wave kernel, with
-// predicated edges, where M or N is not a multiple of 256.
-const Pref kPrefF16[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
+// predicated edges, where M or N is not a multiple of 256. The whole-tile
+// kernels (this one, and for INT4 the FP6 pre-pass one) are taken from 144
+// tiles (56% of the CUs) up, the INT4 in-GEMM-conversion one from 192: at
+// 2304^3 .. 3840^3 and {4096 x 2048, 2048 x 4096, 4096 x 2560} on MI355X
+// the 128 x 128 eight-wave kernels win up to 128 tiles (FP16 2816^3: 59.7
+// against 69.7 us) and lose from 144 on (3072^3: 84.6 against 74.1 us;
+// 3840^3: 155.8 against 112.2 us); INT4 in-GEMM conversion against the
+// 64-byte eight-wave kernel: 53.0 against 58.9 us at 169 tiles, 61.9
+// against 68.9 at 196.
+const Pref kPrefF16[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                          {V_PIPE64, 1}};
-const Pref kPrefS8[] = {{V_WIDE, 256}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
+const Pref kPrefS8[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                         {V_PIPE64, 1}};
-const Pref kPrefS4[] = {{V_I4WIDE, 256}, {V_STAGED256_W2X4, 256}, {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 256}, {V_FP6_256_S2, 512}, {V_I4WIDE, 256}, {V_STAGED256_W2X4, 256},
+const Pref kPrefS4[] = {{V_I4WIDE, 192}, {V_STAGED256_W2X4, 256}, {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
+const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 512}, {V_I4WIDE, 192}, {V_STAGED256_W2X4, 256},
                           {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the

@@ -118,6 +118,21 @@ def test_lds_swizzle_is_a_permutation(ch):
         assert sorted(c ^ _swz(ch, q) for c in range(ch)) == list(range(ch))
 
 
+def test_selection_large_tile_threshold():
+    """Whole 256 x 256 tiles from 144 tiles (56% of the 256 CUs) up for FP16,
+    INT8 and INT4 with a workspace; INT4's in-GEMM conversion from 192; the
+    eight-wave 128 x 128 kernels below (measured crossovers on MI355X)."""
+    name = lambda d, M, N, K, ws=False: mp.variant_name(d, mp.select_variant(d, M, N, K, with_ws=ws))
+    for n, tiles in [(2816, 121), (3072, 144), (3328, 169), (3584, 196), (3840, 225)]:
+        big = tiles >= 144
+        for d in ("f16", "s8"):
+            assert name(d, n, n, n) == ("wide256x256_w2x2_k128_m16" if big else "spread128x128_w2x4_k128_s4"), (d, n)
+        assert name("s4", n, n, n, True) == ("fp6wide256x256_w2x2_k128_s3" if big else "spread128x128_w2x4_k64_s4"), n
+        assert name("s4", n, n, n) == ("e2m3wide256x256_w2x2_k256" if tiles >= 192 else "spread128x128_w2x4_k64_s4"), n
+    # 128 tiles of 256 x 256: the 128 x 128 kernels
+    assert name("f16", 4096, 2048, 4096) == "spread128x128_w2x4_k128_s4"
+
+
 def test_selection_at_sweep_sizes():
     """The kernels the sweep runs (chosen from interleaved MI355X timings)."""
     want = {
