@@ -101,9 +101,9 @@ bool supports(int dtype, const Variant &v, int M, int N, int K, const void *A, c
         return true;
     }
     if (v.kind == WIDE || v.kind == WIDE_SK) {
-        // whole 256 x 256 tiles and 128-byte K-slices, 16-byte aligned rows;
-        // the copy buffers span 128 rows of K bytes (32-bit range)
-        if (!v.fn || M % v.bm || N % v.bn) return false;
+        // 128-byte K-slices, 16-byte aligned rows (M and N any); the copy
+        // buffers span 128 rows of K bytes (32-bit range)
+        if (!v.fn) return false;
         const long kb = row_bytes(dtype, K);
         if (kb % v.bkb || 128 * kb > INT_MAX) return false;
         return aligned(A, 16) && aligned(B, 16);
@@ -585,16 +585,19 @@ hipError_t launch(int dtype, const Variant &v, int splits, const SkPlan &sk, int
             sa.counters = reinterpret_cast<int *>(ws.p);
             sa.partials = reinterpret_cast<uint32_t *>(ws.p + plan.data_off);
         }
-        const void *fn = (v.kind == WIDE_SK && epi.out != OUT_PLAIN) ? v.fn_epi : v.fn;
+        // the one-wave-per-SIMD kernel's raw-sum instantiation stores whole
+        // tiles; scaled outputs and ragged edges take its shared epilogue
+        const void *fn =
+            (v.kind == WIDE_SK && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) ? v.fn_epi : v.fn;
         void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &sa, &epi};
         return hipLaunchKernel(fn, dim3(sk.grid), dim3(v.threads), args, 0, stream);
     }
     if (!v.splitk) {
         const void *fn = v.fn;
         // the one-wave-per-SIMD kernels' table entries store raw sums of whole
-        // tiles; scaled outputs (and for INT4 ragged edges) take their
-        // instantiation with the shared epilogue
-        if (v.kind == WIDE && epi.out != OUT_PLAIN) fn = v.fn_epi;
+        // tiles; scaled outputs and ragged edges take their instantiation with
+        // the shared epilogue
+        if (v.kind == WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) fn = v.fn_epi;
         if (v.kind == I4WIDE && (epi.out != OUT_PLAIN || M % v.bm || N % v.bn)) fn = v.fn_epi;
         void *args[] = {&a, &b, &C, &M, &N, &kb, &tiles_m, &tiles_n, &epi};
         return hipLaunchKernel(fn, dim3(tiles_m * tiles_n), dim3(v.threads), args, 0, stream);

@@ -175,8 +175,8 @@ __global__ __launch_bounds__(T::NTHREADS, 1) void tiled_gemm_sk(const uint8_t *_
     pf_store<DT, T>(epi, Cv, acc, tm, tn, M, N);
 }
 
-// Stream-K schedule of the one-wave-per-SIMD kernel (wide_gemm): whole
-// 256 x 256 tiles, grid as for tiled_gemm_sk.
+// Stream-K schedule of the one-wave-per-SIMD kernel (wide_gemm): 256 x 256
+// tiles (ragged edges as there), grid as for tiled_gemm_sk.
 template <int DT, bool PLAIN = true, int AUX = CP_DEFAULT>
 __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm_sk(const uint8_t *__restrict__ A,
                                                                     const uint8_t *__restrict__ B,
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm_sk(const uint8
     int tm, tn;
     grouped_tile(wk.t, tiles_m, tiles_n, 4, tm, tn);
     typename Acc<DT, 16>::type acc[8][8];
-    wide_accumulate<DT, AUX>(lds, A, B, Kb, tm, tn, wk.k0, wk.len, acc);
+    wide_accumulate<DT, AUX>(lds, A, B, M, N, Kb, tm, tn, wk.k0, wk.len, acc);
     // flag in the copy buffers, as in tiled_gemm_sk
     if (wk.u >= 0 &&
         !sk_fixup<out_t, 8, 8, 4, WideCfg::NTHREADS, true>(

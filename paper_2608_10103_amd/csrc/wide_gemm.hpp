@@ -38,7 +38,10 @@
 // A wave's 16 loads of a slice are spread over 32 groups, and each has at
 // least 16 groups to land. Past the end of K the loads fetch the last slice
 // again into a buffer nobody reads (one loop body for every slice).
-// Needs M and N multiples of 256, K bytes a multiple of 128.
+// M and N may be ragged: each panel's buffer bound covers only its rows
+// inside the matrix (loads of rows past it return zeros and touch no
+// memory), and rows and columns past M and N are not stored. K bytes must be
+// a multiple of 128.
 #pragma once
 
 #include "tiled_gemm.hpp"
@@ -126,12 +129,13 @@ __device__ __forceinline__ void wide_groups(const i32x4 (&a)[8], const i32x4 (&b
 }
 
 // Accumulate K-slices [kt0, kt0 + KT) of tile (tm, tn) into acc (zeroed
-// here) with the schedule above. On return every copy has landed and the
-// accumulators are safe to read; the waves may still be reading LDS, so a
-// caller that reuses the buffers for another tile needs a barrier first.
+// here) with the schedule above; A has M rows, B N rows (ragged edges read
+// as zeros). On return every copy has landed and the accumulators are safe
+// to read; the waves may still be reading LDS, so a caller that reuses the
+// buffers for another tile needs a barrier first.
 template <int DT, int AUX>
-__device__ __forceinline__ void wide_accumulate(uint8_t *lds, const uint8_t *A, const uint8_t *B, int Kb,
-                                                int tm, int tn, int kt0, int KT,
+__device__ __forceinline__ void wide_accumulate(uint8_t *lds, const uint8_t *A, const uint8_t *B, int M, int N,
+                                                int Kb, int tm, int tn, int kt0, int KT,
                                                 typename Acc<DT, 16>::type (&acc)[8][8]) {
     typedef WideCfg T;
     typedef typename Acc<DT, 16>::type acc_t;
@@ -147,10 +151,14 @@ __device__ __forceinline__ void wide_accumulate(uint8_t *lds, const uint8_t *A, 
     // B rows [128 (w - 2), ...) otherwise, into copy blocks [16 w, 16 w + 16);
     // the panel starts at slice kt0
     WideCopy c;
-    c.panel = ((wave < 2) ? A + ((size_t)tm * T::BM + wave * 128) * Kb
-                          : B + ((size_t)tn * T::BN + (wave - 2) * 128) * Kb) +
-              (size_t)kt0 * T::BKB;
-    c.bytes = 128 * Kb - kt0 * T::BKB;
+    const int row0 = (wave < 2) ? tm * T::BM + wave * 128 : tn * T::BN + (wave - 2) * 128;
+    c.panel = ((wave < 2) ? A : B) + (size_t)row0 * Kb + (size_t)kt0 * T::BKB;
+    // the panel's rows inside the matrix (0 .. 128): the buffer bound, so
+    // that copies of rows past M (N) read zeros without touching memory
+    // (wave-uniform; kept in a scalar register, or every copy load becomes a
+    // loop over the descriptor values of the wave's lanes)
+    const int rows = min(max(((wave < 2) ? M : N) - row0, 0), 128);
+    c.bytes = __builtin_amdgcn_readfirstlane(rows ? rows * Kb - kt0 * T::BKB : 0);
     c.voff = (uint32_t)((lane / 8) * 16 * Kb + (lane % 8) * 16);
     c.kb = Kb;
     c.dst = lds + wave * 16 * T::BLK;
@@ -213,7 +221,8 @@ __device__ __forceinline__ void wide_accumulate(uint8_t *lds, const uint8_t *A, 
 
 // Accumulators of a finished tile to C. PLAIN: raw sums of a whole tile to
 // the row-major output, stored straight from the accumulators; otherwise the
-// shared epilogue with scales, zero points and output types (see EpiParams).
+// shared epilogue with scales, zero points, output types and ragged edges
+// (see EpiParams).
 template <int DT, bool PLAIN>
 __device__ __forceinline__ void wide_store(const EpiParams &epi, void *Cv,
                                            const typename Acc<DT, 16>::type (&acc)[8][8], int tm, int tn,
@@ -253,7 +262,7 @@ __global__ __launch_bounds__(WideCfg::NTHREADS, 1) void wide_gemm(const uint8_t 
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, 4, tm, tn);
     typename Acc<DT, 16>::type acc[8][8];
-    wide_accumulate<DT, AUX>(lds, A, B, Kb, tm, tn, 0, Kb / WideCfg::BKB, acc);
+    wide_accumulate<DT, AUX>(lds, A, B, M, N, Kb, tm, tn, 0, Kb / WideCfg::BKB, acc);
     wide_store<DT, PLAIN>(epi, Cv, acc, tm, tn, M, N);
 }
 

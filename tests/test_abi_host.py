@@ -152,8 +152,11 @@ def test_selection_at_sweep_sizes():
             assert mp.select_variant(d, n, n, n, with_ws=True) == mp.select_variant(d, n, n, n)
     for n in (512, 1024, 2048):
         assert mp.select_variant("s4", n, n, n, with_ws=True) == mp.select_variant("s4", n, n, n)
-    # FP16 off whole 256 x 256 tiles: the 8-wave kernel with predicated edges
-    assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "pipe256x256_w2x4_k128_s2"
+    # ragged edges: the one-wave-per-SIMD kernel (its panels bounded by the
+    # rows inside the matrix); K off its 128-byte slices: the 64-byte kernels
+    assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "wide256x256_w2x2_k128_m16"
+    assert mp.variant_name("s8", mp.select_variant("s8", 4000, 4400, 6400)) == "wide256x256_w2x2_k128_m16"
+    assert mp.variant_name("s8", mp.select_variant("s8", 8000, 8000, 8000)) == "spread128x128_w2x4_k64_s4"
 
 
 def _e3m2_value(c):
@@ -327,8 +330,8 @@ def test_every_variant_has_a_kernel_source_family():
 
 
 def test_wide_variant_support():
-    """The one-wave-per-SIMD kernel takes whole 256 x 256 tiles and 128-byte
-    K-slices of 16-byte aligned FP16 or INT8 operands, nothing else."""
+    """The one-wave-per-SIMD kernel takes 128-byte K-slices of 16-byte
+    aligned FP16 or INT8 operands, any M and N, nothing else."""
     for dt, e in (("f16", 64), ("s8", 128), ("s4", 256)):
         v = [i for i in range(mp.num_variants(dt)) if mp.variant_name(dt, i) == "wide256x256_w2x2_k128_m16"]
         assert len(v) == 1
@@ -336,8 +339,8 @@ def test_wide_variant_support():
         ok = dt != "s4"
         assert mp.variant_supports(dt, v, 256, 256, e) == ok
         assert mp.variant_supports(dt, v, 8192, 4096, 64 * e) == ok
-        assert not mp.variant_supports(dt, v, 257, 256, e)       # ragged M
-        assert not mp.variant_supports(dt, v, 256, 200, e)       # ragged N
+        assert mp.variant_supports(dt, v, 257, 256, e) == ok      # ragged M
+        assert mp.variant_supports(dt, v, 1, 200, e) == ok        # ragged N, one row
         assert not mp.variant_supports(dt, v, 256, 256, e + 2)   # K off the slice
         assert not mp.variant_supports(dt, v, 256, 256, e, a_ptr=(1 << 20) + 4)  # unaligned A
 

@@ -117,12 +117,13 @@ def _variant_shapes(dtype, v):
         return [(rows, 3 * per_wg + 5, 9 * e), (1, per_wg, e), (rows - 3, 700, 40 * e),
                 (2 * per_wg + 7, rows, 17 * e), (300, 1, 5 * e), (rows // 2 + 1, 64, 3 * e)]
     if name.startswith("wide"):
-        # whole 256 x 256 tiles, 128-byte K-slices (one slice, an odd count,
-        # many); FP16 and INT8 only
+        # 256 x 256 tiles, 128-byte K-slices (one slice, an odd count, many);
+        # ragged edges (panels partly or wholly past M or N); FP16 and INT8
         if dtype == "s4":
             return []
         e = {"f16": 64, "s8": 128}[dtype]
-        return [(256, 256, e), (512, 768, 3 * e), (768, 256, 5 * e), (512, 512, 33 * e), (256, 1024, 2 * e)]
+        return [(256, 256, e), (512, 768, 3 * e), (768, 256, 5 * e), (512, 512, 33 * e), (256, 1024, 2 * e),
+                (257, 513, 2 * e), (1, 255, e), (300, 77, 3 * e), (600, 700, 5 * e), (129, 1000, 4 * e)]
     if name.startswith("e2m3"):
         # INT4 with the conversion inside the GEMM: K a multiple of 256 (two
         # slices per loop iteration: 1, 5 and 8 iterations), ragged M and N
@@ -667,6 +668,8 @@ SK_CASES = [
     ("s4", SK_F6, 6144, 6400, 32768),      # 600 tiles: 88 in 2 parts
     ("s4", SK_F6, 4000, 4400, 32768),      # ragged edges (shared epilogue), 288 tiles
     ("s4", SK_F6, 1000, 700, 30000),       # 12 tiles, all split; K padded to 30208
+    ("f16", SK_WIDE, 4300, 4100, 4096),    # ragged edges: 289 tiles, 33 in 4 parts
+    ("s8", SK_WIDE, 4300, 4100, 8192),
     ("f16", SK_W8, 2100, 2000, 3200),      # 272 tiles of 128 x 128, 3 parts
     ("s8", SK_W8, 2100, 2000, 8192),
     ("s4", SK_W8K64, 2100, 2000, 12800),   # 64-byte slices

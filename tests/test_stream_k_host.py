@@ -153,8 +153,9 @@ def test_sk_schedule_errors():
     assert L.mpgemm_sk_schedule(0, v, 4352, 4096, 512, None, p, p) == 1
     assert L.mpgemm_sk_schedule(0, -1, 4352, 4096, 512, p, p, p) == 1
     assert L.mpgemm_sk_schedule(7, v, 4352, 4096, 512, p, p, p) == 1
-    # the one-wave-per-SIMD kernel needs whole tiles; it has no INT4 kernel
-    assert L.mpgemm_sk_schedule(0, v, 4353, 4096, 512, p, p, p) == 1
+    # the one-wave-per-SIMD kernel needs 128-byte K-slices; it has no INT4 kernel
+    assert L.mpgemm_sk_schedule(0, v, 4353, 4096, 520, p, p, p) == 1
+    assert L.mpgemm_sk_schedule(0, v, 4353, 4096, 512, p, p, p) == 0
     assert L.mpgemm_sk_schedule(2, _variant("s4", SK_NAMES[0]), 4352, 4096, 512, p, p, p) == 1
     # the FP6 kernel: INT4 only, even K
     f6 = _variant("s4", SK_NAMES[3])
@@ -171,7 +172,7 @@ def test_sk_selection_with_a_workspace():
     for d, M, N, K, plain, twin in [
         ("f16", 4352, 4096, 8192, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
         ("s8", 4352, 4096, 16384, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
-        ("f16", 4000, 4400, 6400, "pipe256x256_w2x4_k128_s2", "pipe256x256_w2x4_k128_s2_sk"),
+        ("f16", 4000, 4400, 6400, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
         ("s8", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
         ("s4", 2100, 2000, 12800, "spread128x128_w2x4_k64_s4", "spread128x128_w2x4_k64_s4_sk"),
         ("f16", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
