@@ -223,41 +223,6 @@ SkPlan sk_plan(int dtype, const Variant &v, int M, int N, int K) {
     return SkPlan{true, (int)dp, (int)parts, (int)(dp + r * parts)};
 }
 
-// Narrow-tile variants (select_narrow): three tiles with the small side on
-// A's rows, then the same three mirrored.
-constexpr int V_NARROW = 44;  // spread32x64_w1x2_k128_s4_m16, 32x128, 64x128; 64x32, 128x32, 128x64
-constexpr int kNumNarrow = 6;
-
-bool is_narrow(int dtype, const Variant &v) {
-    const Variant *t = table(dtype) + V_NARROW;
-    return &v >= t && &v < t + kNumNarrow;
-}
-
-// Splits the entry points use. Only skinny problems (M or N at most 128, the
-// LLM-inference shapes) are split: they stream one large operand from HBM,
-// and splitting K lets more CUs stream it. Measured on MI355X at M = 16,
-// N = K = 8192: FP16 51 -> 38 us with 4 ranges, INT8 28 -> 26 us with 2; for
-// square problems with too few tiles the fixup (partials written back to L2
-// with a device-scope release) costs more than the extra parallelism gains
-// (N = 1024: 11 -> 15 us with 2 ranges), so they are not split. Each range
-// keeps at least 8 slices. The narrow tiles split only while the grid stays
-// within 128 workgroups (at 32 x 8192 x 8192 FP16 with 32 x 128 tiles:
-// 27.4 us with 2 ranges, 30.5 us with 4; INT8 with 32 x 64 tiles: 17.6 us
-// unsplit, 22.1 us with 2).
-int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
-    if (!v.splitk || v.kind != TILED) return 1;
-    if (M > 128 && N > 128 && !is_narrow(dtype, v)) return 1;
-    const bool narrow = is_narrow(dtype, v);
-    const int most = narrow ? 4 : (dtype == F16 ? 4 : 2);
-    const long tiles = tile_count(v, M, N);
-    const long slices = row_bytes(dtype, K) / v.bkb;
-    int s = 1;
-    while ((narrow ? tiles * 2 * s <= 128 : tiles * s < 256) && 2 * s <= most && slices % (2 * s) == 0 &&
-           slices / (2 * s) >= 8 && splits_ok(dtype, v, M, N, K, 2 * s))
-        s *= 2;
-    return s;
-}
-
 // Variant indices in the tables above that the selection uses.
 enum : int {
     V_PIPE256_W2X4 = 9,      // pipe256x256_w2x4_k128_s2
@@ -308,6 +273,57 @@ int sk_base(int variant) {
         case V_FP6_WIDE_SK: return V_FP6_WIDE;
         default: return -1;
     }
+}
+
+// Narrow-tile variants (select_narrow): three tiles with the small side on
+// A's rows, then the same three mirrored; and three with more waves (64 x 64,
+// 64 x 128 and its mirror).
+constexpr int V_NARROW = 44;  // spread32x64_w1x2_k128_s4_m16, 32x128, 64x128; 64x32, 128x32, 128x64
+constexpr int kNumNarrow = 6;
+constexpr int V_NARROW64 = 56;      // spread64x64_w2x2_k128_s4_m16
+constexpr int V_NARROW64W8 = 57;    // spread64x128_w2x4_k128_s4; then its mirror 128 x 64
+constexpr int kNumNarrowW = 3;
+
+// Problems the narrow tiles serve: at most 256 rows on one side, at least
+// 1024 on the other.
+bool narrow_shape(int M, int N) {
+    const int small = M < N ? M : N, large = M < N ? N : M;
+    return small <= 256 && large >= 1024;
+}
+
+// Variants split by the narrow tiles' rule (choose_splits): the narrow tiles,
+// and on narrow shapes the eight-wave 128 x 128 kernel they compete with.
+bool is_narrow(int dtype, const Variant &v, int M, int N) {
+    const Variant *t = table(dtype);
+    if ((&v >= t + V_NARROW && &v < t + V_NARROW + kNumNarrow) ||
+        (&v >= t + V_NARROW64 && &v < t + V_NARROW64 + kNumNarrowW))
+        return true;
+    return &v == t + V_SPREAD128W8 && narrow_shape(M, N);
+}
+
+// Splits the entry points use. Only skinny problems (M or N at most 128, the
+// LLM-inference shapes) are split: they stream one large operand from HBM,
+// and splitting K lets more CUs stream it. Measured on MI355X at M = 16,
+// N = K = 8192: FP16 51 -> 38 us with 4 ranges, INT8 28 -> 26 us with 2; for
+// square problems with too few tiles the fixup (partials written back to L2
+// with a device-scope release) costs more than the extra parallelism gains
+// (N = 1024: 11 -> 15 us with 2 ranges), so they are not split. Each range
+// keeps at least 8 slices. The narrow tiles split only while the grid stays
+// within 128 workgroups (at 32 x 8192 x 8192 FP16 with 32 x 128 tiles:
+// 27.4 us with 2 ranges, 30.5 us with 4; INT8 with 32 x 64 tiles: 17.6 us
+// unsplit, 22.1 us with 2).
+int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
+    if (!v.splitk || v.kind != TILED) return 1;
+    if (M > 128 && N > 128 && !is_narrow(dtype, v, M, N)) return 1;
+    const bool narrow = is_narrow(dtype, v, M, N);
+    const int most = narrow ? 4 : (dtype == F16 ? 4 : 2);
+    const long tiles = tile_count(v, M, N);
+    const long slices = row_bytes(dtype, K) / v.bkb;
+    int s = 1;
+    while ((narrow ? tiles * 2 * s <= 128 : tiles * s < 256) && 2 * s <= most && slices % (2 * s) == 0 &&
+           slices / (2 * s) >= 8 && splits_ok(dtype, v, M, N, K, 2 * s))
+        s *= 2;
+    return s;
 }
 
 // Preferred tiled variants per dtype, largest tile first; a candidate is
@@ -386,30 +402,38 @@ int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, 
 
 // Narrow tiles for problems with up to 256 rows on one side (LLM prefill,
 // batched decoding) and at least 1024 on the other, where the streaming
-// kernel is not taken: 32 x 64, 32 x 128 or
-// 64 x 128 tiles (small side first), and above 128 rows also the 128 x 128
-// kernel. These problems stream the operands through LDS at a per-CU rate
-// that varies little between the tiles, so the choice minimises the bytes
-// one CU copies: (tile rows of both operands) x (K range of a workgroup) x
-// (rounds of 256 workgroups). Within 10% of the minimum, long rows (at least
-// 12 KiB) take the largest tile (fewer, longer workgroups amortise the
-// per-slice overhead) and short rows the most workgroups. Measured on MI355X
-// at 1..256 x {4096, 8192, 11008, 14336, 28672} x {2048 .. 14336} against the
+// kernel is not taken: 32 x 64, 32 x 128, 64 x 64 or 64 x 128 tiles (small
+// side first; the last two with four and eight waves of 32 x 32), and above
+// 64 rows also the eight-wave 128 x 128 kernel (split by the same rule).
+// These problems stream the operands through LDS at a per-CU rate that
+// varies little between the tiles, so the choice minimises the bytes one CU
+// copies: (tile rows of both operands) x (K range of a workgroup) x (rounds
+// of 256 workgroups). Within 10% of the minimum, long rows (at least 12 KiB)
+// take the largest tile (fewer, longer workgroups amortise the per-slice
+// overhead) and short rows the most workgroups. Measured on MI355X at
+// 1..256 x {4096, 8192, 11008, 14336, 28672} x {2048 .. 14336} against the
 // 128x128 split-K kernel: FP16 1.1-1.7x, INT8 1.1-1.5x, INT4 1.1-1.5x faster.
-// With select_skinny, the pick is within 15% of the fastest kernel measured
-// at 102 of 106 shapes (at most 1.32x slower: 48 x 11008 x 4096). Negative:
-// not taken.
+// With the 64 x 64 and eight-wave tiles the pick is within 1.5% of the
+// fastest kernel measured (every candidate at 1, 2 and 4 K-ranges) on
+// average over 30 LLM shapes, at most 1.13x (INT8 256 x 4096 x 14336),
+// against 10% on average for the three-tile set before (FP16 256 x 4096 x
+// 14336: 72.4 -> 53.9 us; INT8 128 x 28672 x 8192: 58.2 -> 46.9 us).
+// Negative: not taken.
 int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
-    const int small = M < N ? M : N, large = M < N ? N : M;
-    if (small > 256 || large < 1024) return -1;
+    const int small = M < N ? M : N;
+    if (!narrow_shape(M, N)) return -1;
     const Variant *t = table(dtype);
     const long kb = row_bytes(dtype, K);
-    int cands[4], nc = 0;
-    for (int i = 0; i < 3; ++i) cands[nc++] = V_NARROW + i + (M <= N ? 0 : 3);
-    if (small > 128) cands[nc++] = V_SPREAD128_K128;
+    int cands[5], nc = 0;
+    const int mir = M <= N ? 0 : 3;
+    cands[nc++] = V_NARROW + mir;                       // 32 x 64 (64 x 32)
+    cands[nc++] = V_NARROW + 1 + mir;                   // 32 x 128 (128 x 32)
+    cands[nc++] = V_NARROW64;                           // 64 x 64
+    cands[nc++] = V_NARROW64W8 + (M <= N ? 0 : 1);      // 64 x 128 (128 x 64), eight waves
+    if (small > 64) cands[nc++] = V_SPREAD128W8;        // 128 x 128, eight waves
     int best = -1;
-    double best_cost = 0, costs[4];
-    long wgs[4];
+    double best_cost = 0, costs[5];
+    long wgs[5];
     for (int i = 0; i < nc; ++i) {
         const Variant &v = t[cands[i]];
         costs[i] = -1;

@@ -51,6 +51,11 @@ typedef TileCfg<64, 128, 2, 2, 128, 4, 4> T64x128_w4;
 typedef TileCfg<64, 32, 2, 1, 128, 4, 4, 16> T64x32_w2_m16;
 typedef TileCfg<128, 32, 4, 1, 128, 4, 4, 16> T128x32_w4_m16;
 typedef TileCfg<128, 64, 2, 2, 128, 4, 4> T128x64_w4;
+// more waves on the narrow tiles: 64 x 64 (four of 32 x 32, 16x16 MFMAs),
+// 64 x 128 and its mirror (eight of 32 x 32)
+typedef TileCfg<64, 64, 2, 2, 128, 4, 4, 16> T64x64_w4_m16;
+typedef TileCfg<64, 128, 2, 4, 128, 4, 4> T64x128_w8;
+typedef TileCfg<128, 64, 4, 2, 128, 4, 4> T128x64_w8;
 
 //             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
 typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
@@ -274,6 +279,9 @@ Variant generic(const char *name) {
      wide<DT, CP_NT>("wide256x256_w2x2_k128_m16_nt"),                     \
      pipelined<DT, T128x128_w8_s4, true>("spread128x128_w2x4_k128_s4"),    \
      pipelined<DT, T128x128_w8_k64_s4, true>("spread128x128_w2x4_k64_s4"), \
+     pipelined<DT, T64x64_w4_m16, true>("spread64x64_w2x2_k128_s4_m16"),   \
+     pipelined<DT, T64x128_w8, true>("spread64x128_w2x4_k128_s4"),         \
+     pipelined<DT, T128x64_w8, true>("spread128x64_w4x2_k128_s4"),         \
      wide_sk<DT>("wide256x256_w2x2_k128_m16_sk"),                          \
      pipelined_sk<DT, T256x256_w8_s2, false>("pipe256x256_w2x4_k128_s2_sk"), \
      pipelined_sk<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4_sk"), \
@@ -282,7 +290,7 @@ Variant generic(const char *name) {
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 61;
+constexpr int kNumCommon = 64;
 constexpr int kNumFp6 = 17;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

@@ -94,7 +94,8 @@ def main(argv=None) -> int:
                 else:
                     Bt = Bd.t().contiguous()
                 runs.append(("bt", None, "transposed B (mpgemm_gemm_bt)"))
-            if args.vendor and dt in ("f16", "s8"):
+            # (torch._int_mm takes more than 16 rows of A only)
+            if args.vendor and (dt == "f16" or (dt == "s8" and M > 16)):
                 runs.append(("vendor", None, "vendor library (A x B^T)"))
             if not runs:
                 continue
