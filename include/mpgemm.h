@@ -248,7 +248,8 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
  * the narrow tiles (at most 256 rows on one side, at least 1024 on the other)
  * while the grid stays within 128 workgroups, up to 4 ranges; where those do
  * not apply, the 128x128 tiles of problems with M or N at most 128 up to 256
- * workgroups, 4 ranges for FP16, 2 for the integer types. */
+ * workgroups, 4 ranges for FP16, 2 for the integer types. The narrow tiles
+ * with an eight-slice ring ("..._s8_m16") are never split. */
 
 /* Splits the automatic choice uses for this variant and problem when a large
  * enough workspace is given (1 = none), or -1 for an invalid dtype, variant

@@ -283,6 +283,10 @@ constexpr int kNumNarrow = 6;
 constexpr int V_NARROW64 = 56;      // spread64x64_w2x2_k128_s4_m16
 constexpr int V_NARROW64W8 = 57;    // spread64x128_w2x4_k128_s4; then its mirror 128 x 64
 constexpr int kNumNarrowW = 3;
+// The same narrow tiles with an eight-slice ring, never split: 32 x 64,
+// 32 x 128, their mirrors 64 x 32 and 128 x 32, then 64 x 64.
+constexpr int V_DEEP = 59;          // spread32x64_w1x2_k128_s8_m16
+constexpr int kNumDeep = 5;
 
 // Problems the narrow tiles serve: at most 256 rows on one side, at least
 // 1024 on the other.
@@ -301,6 +305,11 @@ bool is_narrow(int dtype, const Variant &v, int M, int N) {
     return &v == t + V_SPREAD128W8 && narrow_shape(M, N);
 }
 
+bool is_deep(int dtype, const Variant &v) {
+    const Variant *t = table(dtype);
+    return &v >= t + V_DEEP && &v < t + V_DEEP + kNumDeep;
+}
+
 // Splits the entry points use. Only skinny problems (M or N at most 128, the
 // LLM-inference shapes) are split: they stream one large operand from HBM,
 // and splitting K lets more CUs stream it. Measured on MI355X at M = 16,
@@ -311,9 +320,10 @@ bool is_narrow(int dtype, const Variant &v, int M, int N) {
 // keeps at least 8 slices. The narrow tiles split only while the grid stays
 // within 128 workgroups (at 32 x 8192 x 8192 FP16 with 32 x 128 tiles:
 // 27.4 us with 2 ranges, 30.5 us with 4; INT8 with 32 x 64 tiles: 17.6 us
-// unsplit, 22.1 us with 2).
+// unsplit, 22.1 us with 2). The narrow tiles with the eight-slice ring are
+// never split: their deeper ring is what the split bought.
 int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
-    if (!v.splitk || v.kind != TILED) return 1;
+    if (!v.splitk || v.kind != TILED || is_deep(dtype, v)) return 1;
     if (M > 128 && N > 128 && !is_narrow(dtype, v, M, N)) return 1;
     const bool narrow = is_narrow(dtype, v, M, N);
     const int most = narrow ? 4 : (dtype == F16 ? 4 : 2);
@@ -376,8 +386,8 @@ const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 512}, {V_I4WIDE, 192
 // Streaming kernel for problems with a small side (LLM decoding), against the
 // narrow tiles below (measured on MI355X at 1..32 x {4096, 8192, 14336,
 // 28672} x {4096, 8192, 14336}). It is the faster one while its workgroups
-// stay few and long: up to 8 rows (FP16) or 12 (INT8) with a large side of at
-// most 8192, 16 rows with at most 4096, 32 rows for INT4; with a larger large
+// stay few and long: up to 7 rows (FP16, INT8) with a large side of at most
+// 8192, 16 rows with at most 4096, 32 rows for INT4; with a larger large
 // side only when the large operand is small (at most 32 MiB: INT4 at
 // 14336 x 4096) or each wave has at least 32 K-steps (FP16 at K = 16384).
 // Up to 3.7x faster than the 128x128 split-K kernel, 1.1-1.6x faster than
@@ -386,10 +396,12 @@ const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 512}, {V_I4WIDE, 192
 // wave has at most 8 K-steps of 64 bytes or the small side needs two 16-row
 // blocks; with exactly 8 K-steps per wave, one 8-step prefetch group
 // (skinny16x32_k64_d8) is 1.3-1.4x faster than two 4-step ones. Negative:
-// not taken.
+// not taken. From 8 rows at 8192 x 8192 the narrow 32 x 64 tile with the
+// eight-slice ring is faster (FP16 25.1 against 26.9 us, INT8 15.0 against
+// 15.8; at 6 rows 25.2 against 25.0 and 15.0 against 14.8).
 int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const int small = M < N ? M : N, large = M < N ? N : M;
-    const int most = dtype == S4 ? 32 : (large <= 4096 ? 16 : (dtype == F16 ? 8 : 12));
+    const int most = dtype == S4 ? 32 : (large <= 4096 ? 16 : 7);
     if (small > most || large < 1024) return -1;
     const long steps_per_wave = row_bytes(dtype, K) / 64 / SKINNY_WAVES;
     if (large > 8192 && (long)large * row_bytes(dtype, K) > (32l << 20) && steps_per_wave < 32) return -1;
@@ -418,7 +430,10 @@ int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, 
 // average over 30 LLM shapes, at most 1.13x (INT8 256 x 4096 x 14336),
 // against 10% on average for the three-tile set before (FP16 256 x 4096 x
 // 14336: 72.4 -> 53.9 us; INT8 128 x 28672 x 8192: 58.2 -> 46.9 us).
-// Negative: not taken.
+// Where K is long and one round of workgroups holds the tiles, the same
+// tiles with an eight-slice ring, unsplit, take over (below): FP16 16 x
+// 8192 x 8192 27.1 -> 24.9 us, 128 x 8192 x 8192 36.7 -> 30.1 us; INT8
+// 16 x 8192 x 8192 17.1 -> 15.2 us. Negative: not taken.
 int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const int small = M < N ? M : N;
     if (!narrow_shape(M, N)) return -1;
@@ -450,6 +465,31 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
         const bool bigger = (long)v.bm * v.bn > (long)b.bm * b.bn;
         if (kb >= 12288 ? bigger : (wgs[i] > wgs[best] || (wgs[i] == wgs[best] && bigger))) best = i;
     }
+    // The eight-slice ring, unsplit, one workgroup per CU (96 to 160 KiB of
+    // LDS) in a single round: the same tile streams its rows 1.1-1.3x faster
+    // than through the four-slice ring at 16 ... 128 x 8192 x 8192 (FP16,
+    // INT8), so its cost is scaled by 0.7 against the four-slice candidates,
+    // split or not. Measured on MI355X, it gains only up to 128 rows on the
+    // small side (at 256 its tiles copy twice the bytes of the 128 x 128
+    // ones), with at least 64 slices of K and 128 to 256 workgroups, and with
+    // more than 192 only from 128 slices on (224 tiles at 14336 x 4096: 4-6%
+    // slower); INT4, with its nibble unpacking, gained at no measured shape.
+    int deep = -1;
+    double deep_cost = 0;
+    const long slices = kb / 128;
+    if (dtype != S4 && small <= 128 && slices >= 64) {
+        const int dmir = M <= N ? 0 : 2;
+        for (int cand : {V_DEEP + dmir, V_DEEP + 1 + dmir, V_DEEP + 4}) {
+            const Variant &v = t[cand];
+            const long tiles = tile_count(v, M, N);
+            if (tiles < 128 || tiles > 256 || (tiles > 192 && slices < 128) ||
+                !supports(dtype, v, M, N, K, A, B, C))
+                continue;
+            const double c = 0.7 * (v.bm + v.bn) * kb;
+            if (deep < 0 || c < deep_cost) deep = cand, deep_cost = c;
+        }
+    }
+    if (deep >= 0 && deep_cost < best_cost) return deep;
     return cands[best];
 }
 

@@ -56,6 +56,14 @@ typedef TileCfg<128, 64, 2, 2, 128, 4, 4> T128x64_w4;
 typedef TileCfg<64, 64, 2, 2, 128, 4, 4, 16> T64x64_w4_m16;
 typedef TileCfg<64, 128, 2, 4, 128, 4, 4> T64x128_w8;
 typedef TileCfg<128, 64, 4, 2, 128, 4, 4> T128x64_w8;
+// narrow tiles with an eight-slice ring (160 KiB of LDS for 32 x 128): the
+// unsplit kernel keeps seven slices of its rows in flight, what split K
+// bought the four-slice ring by running more workgroups
+typedef TileCfg<32, 64, 1, 2, 128, 8, 4, 16> T32x64_w2_m16_s8;
+typedef TileCfg<32, 128, 1, 4, 128, 8, 4, 16> T32x128_w4_m16_s8;
+typedef TileCfg<64, 32, 2, 1, 128, 8, 4, 16> T64x32_w2_m16_s8;
+typedef TileCfg<128, 32, 4, 1, 128, 8, 4, 16> T128x32_w4_m16_s8;
+typedef TileCfg<64, 64, 2, 2, 128, 8, 4, 16> T64x64_w4_m16_s8;
 
 //             BM   BN  WGM WGN  J STG GROUP_M    (J runs of 32 k per stage)
 typedef F6Cfg<256, 256, 2, 4, 4, 3, 4> F6_256x256_w8_s3;
@@ -282,6 +290,11 @@ Variant generic(const char *name) {
      pipelined<DT, T64x64_w4_m16, true>("spread64x64_w2x2_k128_s4_m16"),   \
      pipelined<DT, T64x128_w8, true>("spread64x128_w2x4_k128_s4"),         \
      pipelined<DT, T128x64_w8, true>("spread128x64_w4x2_k128_s4"),         \
+     pipelined<DT, T32x64_w2_m16_s8, true>("spread32x64_w1x2_k128_s8_m16"),   \
+     pipelined<DT, T32x128_w4_m16_s8, true>("spread32x128_w1x4_k128_s8_m16"), \
+     pipelined<DT, T64x32_w2_m16_s8, true>("spread64x32_w2x1_k128_s8_m16"),   \
+     pipelined<DT, T128x32_w4_m16_s8, true>("spread128x32_w4x1_k128_s8_m16"), \
+     pipelined<DT, T64x64_w4_m16_s8, true>("spread64x64_w2x2_k128_s8_m16"),   \
      wide_sk<DT>("wide256x256_w2x2_k128_m16_sk"),                          \
      pipelined_sk<DT, T256x256_w8_s2, false>("pipe256x256_w2x4_k128_s2_sk"), \
      pipelined_sk<DT, T128x128_w4_s4, true>("spread128x128_w2x2_k128_s4_sk"), \
@@ -290,7 +303,7 @@ Variant generic(const char *name) {
 
 // Number of entries of VARIANT_LIST, and the INT4 table's FP6 variants after
 // them (variants_s4.hip); each table checks its size against these.
-constexpr int kNumCommon = 64;
+constexpr int kNumCommon = 69;
 constexpr int kNumFp6 = 17;
 constexpr int kNumF16 = kNumCommon, kNumS8 = kNumCommon, kNumS4 = kNumCommon + kNumFp6;
 

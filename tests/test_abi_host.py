@@ -225,16 +225,16 @@ def test_fp6_wide_workspace_offset_bound():
 
 
 def test_skinny_selection():
-    """The streaming kernel while its workgroups stay few and long: up to 8
-    rows (FP16) or 12 (INT8) on the small side with 1024..8192 on the large
-    one, 16 rows with at most 4096, 32 rows for INT4; with a larger large side
+    """The streaming kernel while its workgroups stay few and long: up to 7
+    rows (FP16, INT8) on the small side with 1024..8192 on the large one, 16
+    rows with at most 4096, 32 rows for INT4; with a larger large side
     only for a large operand of at most 32 MiB or at least 32 K-steps per wave.
     16 large-side rows per workgroup with more than 8 K-steps of 64 bytes per
     wave, 32 with fewer, one 8-step prefetch group with exactly 8; never
     split."""
     name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
     for dt in ("f16", "s8", "s4"):
-        for M in (1, 7, 8):
+        for M in (1, 7) if dt != "s4" else (1, 7, 8):
             assert name(dt, M, 8192, 8192).startswith("skinny16x"), (dt, M)
             assert name(dt, 8192, M, 8192).startswith("skinny16x"), (dt, M)  # small N: operands swapped
             v = mp.select_variant(dt, M, 8192, 8192)
@@ -242,11 +242,12 @@ def test_skinny_selection():
         assert name(dt, 16, 4096, 4096).startswith("skinny16x")
         assert not name(dt, 16, 1000, 8192).startswith("skinny")  # large side too small
         assert not name(dt, 8, 8192, 8192, a_ptr=(1 << 20) + 4).startswith("skinny")  # unaligned A
-    assert name("f16", 8, 8192, 8192) == "skinny16x16_k64"       # 32 K-steps per wave
-    assert name("f16", 8, 8192, 2048) == "skinny16x32_k64_d8"    # 8 K-steps per wave
-    assert not name("f16", 9, 8192, 8192).startswith("skinny")
-    assert name("s8", 12, 8192, 8192) == "skinny16x16_k64"       # 16 K-steps per wave
-    assert not name("s8", 13, 8192, 8192).startswith("skinny")
+    assert name("f16", 7, 8192, 8192) == "skinny16x16_k64"       # 32 K-steps per wave
+    assert name("f16", 7, 8192, 2048) == "skinny16x32_k64_d8"    # 8 K-steps per wave
+    assert name("s8", 7, 8192, 8192) == "skinny16x16_k64"        # 16 K-steps per wave
+    for dt in ("f16", "s8"):  # from 8 rows the narrow tile with the eight-slice ring
+        assert name(dt, 8, 8192, 8192) == "spread32x64_w1x2_k128_s8_m16"
+        assert name(dt, 8192, 12, 8192) == "spread64x32_w2x1_k128_s8_m16"
     assert name("s8", 16, 4096, 4096) == "skinny16x32_k64_d8"    # 8 K-steps per wave
     assert name("s8", 16, 4096, 2048) == "skinny16x32_k64"       # 4 K-steps per wave
     assert name("s4", 16, 8192, 8192) == "skinny16x32_k64_d8"    # 8 K-steps per wave
@@ -269,23 +270,32 @@ def test_narrow_selection():
     below were each within 13% of the fastest candidate measured on MI355X
     (every narrow tile at 1, 2 and 4 K-ranges)."""
     name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
-    # the tile that copies the fewest bytes per CU (32 x 128: 64 tiles, 2
-    # K-ranges; 32 x 64: 128 tiles; 64 x 128: 64 tiles, 2 K-ranges)
-    assert name("f16", 16, 8192, 8192) == "spread32x128_w1x4_k128_s4_m16"
-    assert name("f16", 32, 8192, 8192) == "spread32x128_w1x4_k128_s4_m16"
+    # the tile that copies the fewest bytes per CU (32 x 64: 224 tiles;
+    # 64 x 128: 32 tiles, 4 K-ranges)
     assert name("f16", 1, 14336, 4096) == "spread32x64_w1x2_k128_s4_m16"   # 224 tiles
     assert name("s8", 32, 14336, 4096) == "spread32x64_w1x2_k128_s4_m16"
     assert name("s4", 64, 8192, 8192) == "spread32x64_w1x2_k128_s4_m16"    # 256 tiles
-    assert name("f16", 64, 8192, 8192) == "spread64x128_w2x4_k128_s4"      # 64 tiles, 2 K-ranges
     assert name("f16", 64, 4096, 14336) == "spread64x128_w2x4_k128_s4"     # 32 tiles, 4 K-ranges
-    want = {  # (M, N, K): f16, s8, s4
-        (128, 8192, 8192): ("spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16", "spread64x64_w2x2_k128_s4_m16"),
-        (8192, 128, 8192): ("spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16", "spread64x64_w2x2_k128_s4_m16"),
+    # the eight-slice ring, unsplit, where K is long (at least 64 slices) and
+    # 128..256 tiles fill one round: 32 x 64 with 128 or 256 tiles (FP16
+    # 16 x 8192 x 8192: 24.9 against 27.1 us for 32 x 128 in 2 K-ranges)
+    for M in (16, 32, 64):
+        assert name("f16", M, 8192, 8192) == "spread32x64_w1x2_k128_s8_m16", M
+    assert name("s8", 16, 8192, 8192) == "spread32x64_w1x2_k128_s8_m16"
+    assert name("s8", 64, 8192, 8192) == "spread64x64_w2x2_k128_s8_m16"   # 256 tiles of 32 x 64: 64 slices too few
+    assert name("f16", 16, 8192, 16384) == "spread32x64_w1x2_k128_s8_m16"
+    assert name("f16", 16, 14336, 4096) == "spread32x64_w1x2_k128_s4_m16"  # 224 tiles of 64 slices
+    assert name("f16", 32, 28672, 8192) == "spread32x128_w1x4_k128_s8_m16"  # 224 tiles of 128 slices
+    want = {  # (M, N, K): f16, s8, s4 (INT4 never takes the eight-slice ring)
+        (128, 8192, 8192): ("spread64x64_w2x2_k128_s8_m16", "spread64x64_w2x2_k128_s4_m16", "spread64x64_w2x2_k128_s4_m16"),
+        (8192, 128, 8192): ("spread64x64_w2x2_k128_s8_m16", "spread64x64_w2x2_k128_s4_m16", "spread64x64_w2x2_k128_s4_m16"),
+        (8192, 32, 8192): ("spread64x32_w2x1_k128_s8_m16", "spread64x32_w2x1_k128_s8_m16", "skinny32x32_k64"),
         (256, 8192, 8192): ("spread64x128_w2x4_k128_s4",) * 3,
         (8192, 256, 8192): ("spread128x64_w4x2_k128_s4",) * 3,
         (64, 14336, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
         (128, 28672, 8192): ("spread128x128_w2x4_k128_s4",) * 3,   # 224 tiles beat 448
         (256, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 3,
+        (256, 4096, 14336): ("spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16"),
     }
     for (M, N, K), names in want.items():
         assert tuple(name(dt, M, N, K) for dt in ("f16", "s8", "s4")) == names, (M, N, K)
@@ -294,7 +304,11 @@ def test_narrow_selection():
         assert name(dt, 64, 1000, 8192).startswith("spread128")  # large side too small
         assert name(dt, 64, 8192, 8192 - 8).startswith("generic") or \
             name(dt, 64, 8192, 8192 - 8).startswith("spread128")  # K off the 128-byte slice
-    assert name("s8", 8192, 64, 8192) == "spread64x32_w2x1_k128_s4_m16"
+    assert name("s8", 8192, 64, 8192) == "spread64x64_w2x2_k128_s8_m16"
+    for dt in ("f16", "s8"):  # the eight-slice ring is never split
+        for v in range(mp.num_variants(dt)):
+            if "_s8_m16" in mp.variant_name(dt, v):
+                assert mp.select_splits(dt, v, 16, 8192, 8192) == 1
 
 
 def test_split_k_selection():
@@ -314,13 +328,16 @@ def test_split_k_selection():
         v = mp.select_variant(dt, 64, 8192, 1024)
         assert mp.select_splits(dt, v, 64, 8192, 1024) <= most  # every range keeps >= 8 slices
     sel = lambda dt, M, N, K: mp.select_splits(dt, mp.select_variant(dt, M, N, K), M, N, K)
-    assert sel("f16", 32, 8192, 8192) == 2     # 64 tiles of 32 x 128
-    assert sel("f16", 8192, 32, 8192) == 2
-    assert sel("f16", 64, 8192, 8192) == 2     # 64 tiles of 64 x 128
-    assert sel("f16", 128, 8192, 8192) == 2    # 64 tiles of 128 x 128: the narrow tiles' rule
+    split = lambda dt, name, M, N, K: mp.select_splits(
+        dt, [v for v in range(mp.num_variants(dt)) if mp.variant_name(dt, v) == name][0], M, N, K)
+    assert split("f16", "spread32x128_w1x4_k128_s4_m16", 32, 8192, 8192) == 2  # 64 tiles
+    assert split("f16", "spread128x32_w4x1_k128_s4_m16", 8192, 32, 8192) == 2
+    assert split("f16", "spread64x128_w2x4_k128_s4", 64, 8192, 8192) == 2      # 64 tiles
+    assert split("f16", "spread128x128_w2x4_k128_s4", 128, 8192, 8192) == 2   # the narrow tiles' rule
+    assert split("s8", "spread32x128_w1x4_k128_s4_m16", 32, 8192, 8192) == 2
+    assert sel("f16", 32, 8192, 8192) == 1     # the eight-slice ring instead
     assert sel("f16", 256, 4096, 14336) == 2
     assert sel("f16", 64, 4096, 8192) == 4     # 32 tiles
-    assert sel("s8", 32, 8192, 8192) == 2      # 64 tiles of 32 x 128
     assert sel("s8", 32, 14336, 4096) == 1     # 224 tiles of 32 x 64
     assert sel("s8", 128, 8192, 8192) == 1
     assert sel("f16", 256, 8192, 8192) == 1

@@ -140,6 +140,8 @@ def _variant_shapes(dtype, v):
     return [(2 * bm, 3 * bn, 5 * elems_per_kb), (bm, bn, elems_per_kb), (3 * bm, bn, 2 * elems_per_kb),
             # more K-slices than a 4- or 5-deep ring holds, not a multiple of 3
             (bm, 2 * bn, 7 * elems_per_kb),
+            # more than twice what an 8-deep ring holds, ragged edges
+            (bm + 3, 2 * bn - 1, 19 * elems_per_kb),
             # ragged M and N: predicated edge tiles
             (2 * bm + 17, bn + 5, 3 * elems_per_kb), (1, bn - 1, elems_per_kb), (bm + 31, 1, 2 * elems_per_kb)]
 
@@ -578,6 +580,8 @@ def test_llm_inference_shapes(dtype):
                       (256, 4096, 4096), (16, 14336, 4096), (7, 1000, 2048),
                       # the narrow tiles, mirrored when N is the small side
                       (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024),
+                      # the narrow tiles with the eight-slice ring (FP16, INT8), ragged sides
+                      (9, 8192, 8192), (16, 8192, 4096), (8192, 16, 4096), (8192, 100, 8192),
                       # 272 tiles of 128 x 128: stream-K with a workspace
                       (2100, 2000, 6400)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
