@@ -264,11 +264,12 @@ def test_skinny_selection():
 
 
 def test_narrow_selection():
-    """17..256 rows on one side (past the streaming kernel) and at least 1024
+    """8..512 rows on one side (past the streaming kernel) and at least 1024
     on the other: the narrow tiles, small side first; mirrored when N is the
-    small side; from 65 rows also the eight-wave 128 x 128 kernel. The picks
-    below were each within 13% of the fastest candidate measured on MI355X
-    (every narrow tile at 1, 2 and 4 K-ranges)."""
+    small side; from 65 rows also the eight-wave 128 x 128 kernel (for INT4
+    its 64-byte-slice form). The picks below were each within 16% of the
+    fastest candidate measured on MI355X (every narrow tile at 1, 2 and 4
+    K-ranges)."""
     name = lambda dt, M, N, K, **kw: mp.variant_name(dt, mp.select_variant(dt, M, N, K, **kw))
     # the tile that copies the fewest bytes per CU (32 x 64: 224 tiles;
     # 64 x 128: 32 tiles, 4 K-ranges)
@@ -293,14 +294,23 @@ def test_narrow_selection():
         (256, 8192, 8192): ("spread64x128_w2x4_k128_s4",) * 3,
         (8192, 256, 8192): ("spread128x64_w4x2_k128_s4",) * 3,
         (64, 14336, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
-        (128, 28672, 8192): ("spread128x128_w2x4_k128_s4",) * 3,   # 224 tiles beat 448
-        (256, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 3,
+        # 224 tiles beat 448; INT4 takes the 64-byte-slice 128 x 128 kernel
+        (128, 28672, 8192): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
+        (256, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
+        # 257 .. 512 rows (measured at 320, 384, 512 x 2048 .. 14336 x 2048 ..
+        # 8192: 1.13x / 1.15x / 1.21x faster on average than the 128 x 128
+        # kernel taken before, FP16 / INT8 / INT4)
+        (512, 4096, 4096): ("spread64x128_w2x4_k128_s4",) * 3,
+        (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
+        (384, 2048, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
+        (512, 2048, 8192): ("spread128x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         (256, 4096, 14336): ("spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16"),
     }
     for (M, N, K), names in want.items():
         assert tuple(name(dt, M, N, K) for dt in ("f16", "s8", "s4")) == names, (M, N, K)
     for dt in ("f16", "s8", "s4"):
-        assert not name(dt, 257, 8192, 8192).startswith(("spread32", "spread64"))
+        assert not name(dt, 513, 4096, 4096).startswith(("spread32", "spread64"))  # past the narrow tiles
         assert name(dt, 64, 1000, 8192).startswith("spread128")  # large side too small
         assert name(dt, 64, 8192, 8192 - 8).startswith("generic") or \
             name(dt, 64, 8192, 8192 - 8).startswith("spread128")  # K off the 128-byte slice

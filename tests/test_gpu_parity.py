@@ -582,6 +582,8 @@ def test_llm_inference_shapes(dtype):
                       (48, 4096, 2048), (2048, 48, 2048), (4096, 128, 1024), (200, 2048, 1024),
                       # the narrow tiles with the eight-slice ring (FP16, INT8), ragged sides
                       (9, 8192, 8192), (16, 8192, 4096), (8192, 16, 4096), (8192, 100, 8192),
+                      # 257 .. 512 rows: narrow tiles in place of 128 x 128
+                      (384, 2048, 4096), (4096, 500, 4096), (320, 4096, 2048),
                       # 272 tiles of 128 x 128: stream-K with a workspace
                       (2100, 2000, 6400)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
