@@ -520,6 +520,20 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         for (int cand : {V_SPREAD128_K128, V_SPREAD128_K64})
             if (supports(dtype, t[cand], M, N, K, A, B, C)) return cand;
     }
+    // FP16 with a workspace, 96 to 143 tiles of 256 x 256 and at least 128
+    // K-slices: the one-wave-per-SIMD kernel under its stream-K schedule
+    // (each tile in parts, so every CU has work) beats the eight-wave
+    // 128 x 128 kernel the preferences give below 144 tiles: 768 x 8192 x
+    // 8192 126.2 against 142.1 us, 1024 x 8192 x 8192 150.5 against 155.6 (its
+    // own stream-K twin), 2560 x 2560 x 8192 127.2 against 135.8; with 64
+    // tiles, fewer slices or INT8 it does not.
+    if (dtype == F16 && with_ws) {
+        const Variant &w = t[V_WIDE_SK];
+        const long wt = tile_count(w, M, N);
+        if (wt >= 96 && wt < 144 && row_bytes(dtype, K) / w.bkb >= 128 && supports(dtype, w, M, N, K, A, B, C) &&
+            sk_plan(dtype, w, M, N, K).on)
+            return V_WIDE_SK;
+    }
     const bool s4ws = dtype == S4 && with_ws;
     const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : (s4ws ? kPrefS4Ws : kPrefS4));
     const int n = dtype == F16 ? (int)(sizeof(kPrefF16) / sizeof(Pref))

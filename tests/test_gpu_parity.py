@@ -760,6 +760,20 @@ def test_stream_k_through_the_entry_point(dtype, K):
                   f"stream-K entry point {dtype} {M}x{N}x{K}")
 
 
+def test_stream_k_wide_below_a_round_fp16():
+    """FP16 with a workspace, 96 tiles of 256 x 256 and 128 K-slices: the
+    entry point takes the one-wave-per-SIMD kernel's stream-K schedule over
+    the 128 x 128 kernel, and matches the oracle on sampled rows."""
+    M, N, K = 768, 8192, 8192
+    v = mp.select_variant("f16", M, N, K, with_ws=True)
+    assert mp.variant_name("f16", v) == "wide256x256_w2x2_k128_m16_sk"
+    A, B = si.gen_operands("f16", M, N, K, seed=77)
+    C = mp.GEMM["f16"](dev(A), dev(B), workspace="auto")
+    rows = np.array([0, 1, 255, 256, 511, 767])
+    assert_parity("f16", C.cpu().numpy()[rows], *oracle_gemm("f16", A, B, rows=rows), "stream-K wide f16 768")
+    _log(f"stream-K wide below a round: {mp.sk_schedule('f16', v, M, N, K)}")
+
+
 # ---------------------------------------------------------------- scaled outputs (fused epilogue)
 
 from tests.gpu_util import TORCH_OUT, assert_scaled  # noqa: E402

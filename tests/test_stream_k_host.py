@@ -182,6 +182,13 @@ def test_sk_selection_with_a_workspace():
     # schedule off: too few slices, whole rounds, last round over half full
     for d, M, N, K in [("s8", 4352, 4096, 4096), ("f16", 8192, 8192, 8192), ("f16", 5120, 5120, 8192)]:
         assert not name(d, M, N, K, True).endswith("_sk"), (d, M, N, K)
+    # FP16, 96..143 tiles of 256 x 256 and at least 128 K-slices: the
+    # one-wave-per-SIMD kernel's stream-K schedule in place of 128 x 128
+    for M, N, K in [(768, 8192, 8192), (1024, 8192, 8192), (2560, 2560, 8192)]:
+        assert name("f16", M, N, K, False) == "spread128x128_w2x4_k128_s4"
+        assert name("f16", M, N, K, True) == "wide256x256_w2x2_k128_m16_sk", (M, N, K)
+    for d, M, N, K in [("f16", 1024, 4096, 8192), ("f16", 1024, 8192, 4096), ("s8", 768, 8192, 8192)]:
+        assert not name(d, M, N, K, True).startswith("wide"), (d, M, N, K)  # 64 tiles, 64 slices, INT8
     # INT4 with a workspace: the FP6 pre-pass kernel, stream-K where its plan is on
     assert name("s4", 4352, 4096, 16384, True) == "fp6wide256x256_w2x2_k128_s3_sk"
     assert name("s4", 8192, 8192, 8192, True) == "fp6wide256x256_w2x2_k128_s3"
