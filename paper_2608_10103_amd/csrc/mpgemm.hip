@@ -288,11 +288,19 @@ constexpr int kNumNarrowW = 3;
 constexpr int V_DEEP = 59;          // spread32x64_w1x2_k128_s8_m16
 constexpr int kNumDeep = 5;
 
-// Problems the narrow tiles serve: at most 512 rows on one side, at least
-// 1024 on the other.
+// Problems the narrow tiles serve: at most 1024 rows on the small side, and
+// either at least 1024 on the large one with the small side at most 512
+// rows or the large one at least twice as long, or (from 257 rows) 128 x 128
+// tiles that would fill at most a quarter of the CUs (1024 x 1024, 768 x
+// 768: there the 128 x 128 kernel leaves CUs idle and takes up to 2.4x
+// longer with long K, 512 x 512 x 8192 FP16 47.4 against 19.7 us). Larger
+// square-ish problems keep the square choice (at 1536^2 .. 2560^2 the 128 x
+// 128 kernel is 1.2-1.4x faster than the narrow tiles).
 bool narrow_shape(int M, int N) {
     const int small = M < N ? M : N, large = M < N ? N : M;
-    return small <= 512 && large >= 1024;
+    const long tiles128 = (long)((small + 127) / 128) * ((large + 127) / 128);
+    return small <= 1024 && ((large >= 1024 && (small <= 512 || large >= 2 * small)) ||
+                             (small > 256 && tiles128 <= 64));
 }
 
 // The eight-wave 128 x 128 kernel that competes with the narrow tiles: the
@@ -332,6 +340,11 @@ int choose_splits(int dtype, const Variant &v, int M, int N, int K) {
     if (!v.splitk || v.kind != TILED || is_deep(dtype, v)) return 1;
     if (M > 128 && N > 128 && !is_narrow(dtype, v, M, N)) return 1;
     const bool narrow = is_narrow(dtype, v, M, N);
+    // Above 256 rows on the small side the narrow choice runs unsplit: its
+    // best unsplit tile is within 1% of the best split one on average
+    // (320 .. 1024 rows), while the split 128 x 128 kernel the cost model
+    // would take is up to 1.4x slower (FP16 768 x 768 x 8192).
+    if (narrow && (M < N ? M : N) > 256) return 1;
     const int most = narrow ? 4 : (dtype == F16 ? 4 : 2);
     const long tiles = tile_count(v, M, N);
     const long slices = row_bytes(dtype, K) / v.bkb;
@@ -451,8 +464,10 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
     const long kb = row_bytes(dtype, K);
     int cands[5], nc = 0;
     const int mir = M <= N ? 0 : 3;
-    cands[nc++] = V_NARROW + mir;                       // 32 x 64 (64 x 32)
-    cands[nc++] = V_NARROW + 1 + mir;                   // 32 x 128 (128 x 32)
+    if (small <= 256) {  // 32-row tiles: too little work per wave above that
+        cands[nc++] = V_NARROW + mir;                   // 32 x 64 (64 x 32)
+        cands[nc++] = V_NARROW + 1 + mir;               // 32 x 128 (128 x 32)
+    }
     cands[nc++] = V_NARROW64;                           // 64 x 64
     cands[nc++] = V_NARROW64W8 + (M <= N ? 0 : 1);      // 64 x 128 (128 x 64), eight waves
     if (small > 64) cands[nc++] = spread128w8(dtype);   // 128 x 128, eight waves
@@ -510,6 +525,21 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     const Variant *t = table(dtype);
     const int sk = select_skinny(dtype, M, N, K, A, B, C);
     if (sk >= 0) return sk;
+    // FP16 with a workspace, 96 to 143 tiles of 256 x 256 and at least 128
+    // K-slices: the one-wave-per-SIMD kernel under its stream-K schedule
+    // (each tile in parts, so every CU has work) beats the eight-wave
+    // 128 x 128 kernel the preferences give below 144 tiles: 768 x 8192 x
+    // 8192 126.2 against 142.1 us, 1024 x 8192 x 8192 150.5 against 155.6 (its
+    // own stream-K twin), 2560 x 2560 x 8192 127.2 against 135.8; with 64
+    // tiles, fewer slices or INT8 it does not. Checked before the narrow
+    // tiles, which would take 128 x 128 at 768 and 1024 x 8192 x 8192.
+    if (dtype == F16 && with_ws && (M < N ? M : N) > 512) {
+        const Variant &w = t[V_WIDE_SK];
+        const long wt = tile_count(w, M, N);
+        if (wt >= 96 && wt < 144 && row_bytes(dtype, K) / w.bkb >= 128 && supports(dtype, w, M, N, K, A, B, C) &&
+            sk_plan(dtype, w, M, N, K).on)
+            return V_WIDE_SK;
+    }
     const int nv = select_narrow(dtype, M, N, K, A, B, C);
     if (nv >= 0) return nv;
     // Skinny problems (M or N at most 128: LLM-inference shapes) are bound by
@@ -519,20 +549,6 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     if (M <= 128 || N <= 128) {
         for (int cand : {V_SPREAD128_K128, V_SPREAD128_K64})
             if (supports(dtype, t[cand], M, N, K, A, B, C)) return cand;
-    }
-    // FP16 with a workspace, 96 to 143 tiles of 256 x 256 and at least 128
-    // K-slices: the one-wave-per-SIMD kernel under its stream-K schedule
-    // (each tile in parts, so every CU has work) beats the eight-wave
-    // 128 x 128 kernel the preferences give below 144 tiles: 768 x 8192 x
-    // 8192 126.2 against 142.1 us, 1024 x 8192 x 8192 150.5 against 155.6 (its
-    // own stream-K twin), 2560 x 2560 x 8192 127.2 against 135.8; with 64
-    // tiles, fewer slices or INT8 it does not.
-    if (dtype == F16 && with_ws) {
-        const Variant &w = t[V_WIDE_SK];
-        const long wt = tile_count(w, M, N);
-        if (wt >= 96 && wt < 144 && row_bytes(dtype, K) / w.bkb >= 128 && supports(dtype, w, M, N, K, A, B, C) &&
-            sk_plan(dtype, w, M, N, K).on)
-            return V_WIDE_SK;
     }
     const bool s4ws = dtype == S4 && with_ws;
     const Pref *prefs = dtype == F16 ? kPrefF16 : (dtype == S8 ? kPrefS8 : (s4ws ? kPrefS4Ws : kPrefS4));

@@ -139,8 +139,11 @@ def test_selection_at_sweep_sizes():
         8192: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         2048: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
-        1024: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
-        512: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
+        # 64 tiles of 128 x 128 would fill a quarter of the CUs: the narrow
+        # 64 x 64 tiles (FP16 8.0 against 10.3 us, INT8 7.1 against 7.6, INT4
+        # 7.1 against 7.9)
+        1024: ("spread64x64_w2x2_k128_s4_m16",) * 3,
+        512: ("spread64x64_w2x2_k128_s4_m16",) * 3,  # every tile about 7 us here (launch bound)
     }
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
@@ -303,14 +306,19 @@ def test_narrow_selection():
         (512, 4096, 4096): ("spread64x128_w2x4_k128_s4",) * 3,
         (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
         (384, 2048, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
-        (512, 2048, 8192): ("spread128x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        (512, 2048, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,   # unsplit above 256 rows
+        # near-square up to 1024 where 128 x 128 tiles fill at most 64 CUs
+        (1024, 1024, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
+        (768, 768, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,
         (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         (256, 4096, 14336): ("spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16"),
     }
     for (M, N, K), names in want.items():
         assert tuple(name(dt, M, N, K) for dt in ("f16", "s8", "s4")) == names, (M, N, K)
     for dt in ("f16", "s8", "s4"):
-        assert not name(dt, 513, 4096, 4096).startswith(("spread32", "spread64"))  # past the narrow tiles
+        assert not name(dt, 1025, 4096, 4096).startswith(("spread32", "spread64"))  # past the narrow tiles
+        assert not name(dt, 1536, 1536, 1536).startswith(("spread32", "spread64"))  # square: 144 tiles of 128
+        assert mp.select_splits(dt, mp.select_variant(dt, 384, 2048, 8192), 384, 2048, 8192) == 1
         assert name(dt, 64, 1000, 8192).startswith("spread128")  # large side too small
         assert name(dt, 64, 8192, 8192 - 8).startswith("generic") or \
             name(dt, 64, 8192, 8192 - 8).startswith("spread128")  # K off the 128-byte slice
