@@ -288,19 +288,19 @@ constexpr int kNumNarrowW = 3;
 constexpr int V_DEEP = 59;          // spread32x64_w1x2_k128_s8_m16
 constexpr int kNumDeep = 5;
 
-// Problems the narrow tiles serve: at most 1024 rows on the small side, and
-// either at least 1024 on the large one with the small side at most 512
-// rows or the large one at least twice as long, or (from 257 rows) 128 x 128
-// tiles that would fill at most a quarter of the CUs (1024 x 1024, 768 x
-// 768: there the 128 x 128 kernel leaves CUs idle and takes up to 2.4x
-// longer with long K, 512 x 512 x 8192 FP16 47.4 against 19.7 us). Larger
-// square-ish problems keep the square choice (at 1536^2 .. 2560^2 the 128 x
-// 128 kernel is 1.2-1.4x faster than the narrow tiles).
+// Problems the narrow tiles serve: at most 1024 rows on the small side and
+// at least 1024 on the large one, with the small side at most 512 rows or
+// the large one at least twice as long; or, from 257 rows on, any problem
+// whose 128 x 128 tiles would fill fewer than half the CUs (128 tiles).
+// There the 128 x 128 kernel leaves CUs idle: 1280^2 x 4096 FP16 29.8 against
+// 23.7 us with 64 x 128 tiles, 1024^2 x 4096 INT8 16.3 against 11.6 with
+// 64 x 64, 512^2 x 8192 FP16 47.4 against 19.7; from 144 tiles on (1536^2
+// and up) it is 1.2-1.4x faster than any narrow tile.
 bool narrow_shape(int M, int N) {
     const int small = M < N ? M : N, large = M < N ? N : M;
     const long tiles128 = (long)((small + 127) / 128) * ((large + 127) / 128);
-    return small <= 1024 && ((large >= 1024 && (small <= 512 || large >= 2 * small)) ||
-                             (small > 256 && tiles128 <= 64));
+    return (small <= 1024 && large >= 1024 && (small <= 512 || large >= 2 * small)) ||
+           (small > 256 && tiles128 < 128);
 }
 
 // The eight-wave 128 x 128 kernel that competes with the narrow tiles: the

@@ -307,9 +307,11 @@ def test_narrow_selection():
         (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
         (384, 2048, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
         (512, 2048, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,   # unsplit above 256 rows
-        # near-square up to 1024 where 128 x 128 tiles fill at most 64 CUs
+        # from 257 rows, wherever 128 x 128 tiles would fill under half the CUs
         (1024, 1024, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
         (768, 768, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,
+        (1280, 1280, 4096): ("spread64x128_w2x4_k128_s4",) * 3,          # 100 tiles of 128 x 128
+        (1408, 1408, 2048): ("spread64x128_w2x4_k128_s4",) * 3,          # 121
         (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         (256, 4096, 14336): ("spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16"),
     }

@@ -584,6 +584,8 @@ def test_llm_inference_shapes(dtype):
                       (9, 8192, 8192), (16, 8192, 4096), (8192, 16, 4096), (8192, 100, 8192),
                       # 257 .. 512 rows: narrow tiles in place of 128 x 128
                       (384, 2048, 4096), (4096, 500, 4096), (320, 4096, 2048),
+                      # under half the CUs with 128 x 128 tiles: narrow tiles, ragged
+                      (1100, 1300, 2048), (700, 700, 4096),
                       # 272 tiles of 128 x 128: stream-K with a workspace
                       (2100, 2000, 6400)]:
         A, B = si.gen_operands(dtype, M, N, K, seed=M + N + K)
