@@ -468,7 +468,9 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
         cands[nc++] = V_NARROW + mir;                   // 32 x 64 (64 x 32)
         cands[nc++] = V_NARROW + 1 + mir;               // 32 x 128 (128 x 32)
     }
-    cands[nc++] = V_NARROW64;                           // 64 x 64
+    // 64 x 64 (four waves); FP16 above 256 rows does as well or better with
+    // the eight-wave 64 x 128 (512 x 512 x 8192: 19.7 against 25.4 us)
+    if (dtype != F16 || small <= 256) cands[nc++] = V_NARROW64;
     cands[nc++] = V_NARROW64W8 + (M <= N ? 0 : 1);      // 64 x 128 (128 x 64), eight waves
     if (small > 64) cands[nc++] = spread128w8(dtype);   // 128 x 128, eight waves
     int best = -1;

@@ -140,10 +140,10 @@ def test_selection_at_sweep_sizes():
         4096: ("wide256x256_w2x2_k128_m16",) * 2 + ("e2m3wide256x256_w2x2_k256",),
         2048: ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         # 64 tiles of 128 x 128 would fill a quarter of the CUs: the narrow
-        # 64 x 64 tiles (FP16 8.0 against 10.3 us, INT8 7.1 against 7.6, INT4
-        # 7.1 against 7.9)
-        1024: ("spread64x64_w2x2_k128_s4_m16",) * 3,
-        512: ("spread64x64_w2x2_k128_s4_m16",) * 3,  # every tile about 7 us here (launch bound)
+        # tiles (FP16 64 x 128 8.0 against 10.3 us, INT8 64 x 64 7.1 against
+        # 7.6, INT4 7.1 against 7.9)
+        1024: ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        512: ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,  # launch bound, ~7 us
     }
     for n, names in want.items():
         got = tuple(mp.variant_name(d, mp.select_variant(d, n, n, n)) for d in ("f16", "s8", "s4"))
@@ -305,11 +305,12 @@ def test_narrow_selection():
         # kernel taken before, FP16 / INT8 / INT4)
         (512, 4096, 4096): ("spread64x128_w2x4_k128_s4",) * 3,
         (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
-        (384, 2048, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
-        (512, 2048, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,   # unsplit above 256 rows
+        (384, 2048, 4096): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        (512, 2048, 8192): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,  # unsplit
         # from 257 rows, wherever 128 x 128 tiles would fill under half the CUs
-        (1024, 1024, 4096): ("spread64x64_w2x2_k128_s4_m16",) * 3,
-        (768, 768, 8192): ("spread64x64_w2x2_k128_s4_m16",) * 3,
+        # (FP16 above 256 rows: the eight-wave 64 x 128 rather than 64 x 64)
+        (1024, 1024, 4096): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        (768, 768, 8192): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
         (1280, 1280, 4096): ("spread64x128_w2x4_k128_s4",) * 3,          # 100 tiles of 128 x 128
         (1408, 1408, 2048): ("spread64x128_w2x4_k128_s4",) * 3,          # 121
         (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
