@@ -454,8 +454,8 @@ int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, 
 // 8192 x 8192 27.1 -> 24.9 us, 128 x 8192 x 8192 36.7 -> 30.1 us; INT8
 // 16 x 8192 x 8192 17.1 -> 15.2 us. From 257 to 512 rows (the eight-wave
 // 128 x 128 kernel alone before) at 320, 384, 512 x 2048 .. 14336 x 2048 ..
-// 8192 and two mirrored shapes: FP16 1.13x, INT8 1.15x, INT4 1.21x faster
-// (geometric means; up to 1.37x, 1.49x, 1.78x; slower nowhere), the pick
+// 8192 and two mirrored shapes: FP16 1.12x, INT8 1.15x, INT4 1.21x faster
+// (geometric means; up to 1.32x, 1.49x, 1.78x; slower nowhere), the pick
 // within 1.5% of the fastest kernel timed on average. Negative: not taken.
 int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, const void *C) {
     const int small = M < N ? M : N;

@@ -301,7 +301,7 @@ def test_narrow_selection():
         (128, 28672, 8192): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         (256, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
         # 257 .. 512 rows (measured at 320, 384, 512 x 2048 .. 14336 x 2048 ..
-        # 8192: 1.13x / 1.15x / 1.21x faster on average than the 128 x 128
+        # 8192: 1.12x / 1.15x / 1.21x faster on average than the 128 x 128
         # kernel taken before, FP16 / INT8 / INT4)
         (512, 4096, 4096): ("spread64x128_w2x4_k128_s4",) * 3,
         (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
