@@ -431,11 +431,13 @@ int select_skinny(int dtype, int M, int N, int K, const void *A, const void *B, 
     return supports(dtype, table(dtype)[v], M, N, K, A, B, C) ? v : -1;
 }
 
-// Narrow tiles for problems with up to 512 rows on one side (LLM prefill,
-// batched decoding) and at least 1024 on the other, where the streaming
-// kernel is not taken: 32 x 64, 32 x 128, 64 x 64 or 64 x 128 tiles (small
+// Narrow tiles for the problems `narrow_shape` admits (LLM prefill, batched
+// decoding, and problems whose 128 x 128 tiles would leave CUs idle) where
+// the streaming kernel is not taken: 32 x 64, 32 x 128 (up to 256 rows on
+// the small side), 64 x 64 (FP16 up to 256 rows) or 64 x 128 tiles (small
 // side first; the last two with four and eight waves of 32 x 32), and above
-// 64 rows also the eight-wave 128 x 128 kernel (split by the same rule).
+// 64 rows also the eight-wave 128 x 128 kernel (split by the same rule, which
+// splits nothing above 256 rows).
 // These problems stream the operands through LDS at a per-CU rate that
 // varies little between the tiles, so the choice minimises the bytes one CU
 // copies: (tile rows of both operands) x (K range of a workgroup) x (rounds
