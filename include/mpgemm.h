@@ -245,7 +245,7 @@ hipError_t mpgemm_run_variant(int dtype, int variant, int M, int N, int K, const
  * from the unsplit kernel's, within the same error bound; integers: exact).
  * Partials and per-tile counters live in the caller's workspace. With a
  * workspace, the automatic choice splits only problems with a small side:
- * the narrow tiles (at most 512 rows on one side, at least 1024 on the other)
+ * the narrow tiles (at most 256 rows on one side, at least 1024 on the other)
  * while the grid stays within 128 workgroups, up to 4 ranges; where those do
  * not apply, the 128x128 tiles of problems with M or N at most 128 up to 256
  * workgroups, 4 ranges for FP16, 2 for the integer types. The narrow tiles
