@@ -597,6 +597,42 @@ def test_llm_inference_shapes(dtype):
     _log(f"{dtype} LLM shapes: ok")
 
 
+def _random_shapes(seed, n):
+    """Seeded shapes across the automatic choice's regions: the streaming
+    kernel (1..7 rows), narrow and eight-slice narrow tiles (8..1024 rows),
+    tiles leaving CUs idle (up to 1408 square-ish), 128 x 128 and 256 x 256,
+    either side small, ragged sides, K off the big multiples (but on the
+    128-byte grid of every precision, a multiple of 256 elements)."""
+    rng = np.random.default_rng(seed)
+    small = [1, 3, 7, 8, 12, 16, 33, 64, 100, 128, 200, 257, 320, 500, 640, 777, 1000, 1100, 1300]
+    large = [1024, 1500, 2048, 3000, 4096, 5000, 8192]
+    out = []
+    for _ in range(n):
+        a = int(rng.choice(small))
+        b = int(rng.choice(large)) if a <= 1024 else int(rng.integers(a, 1409))
+        K = 256 * int(rng.integers(1, 33))
+        out.append((a, b, K) if rng.random() < 0.6 else (b, a, K))
+    return out
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_automatic_choice_random_shapes(dtype):
+    """Whatever kernel the entry point picks, with and without a workspace,
+    on seeded shapes across every region of the choice: sampled rows against
+    the oracle (first, last and four seeded rows)."""
+    for i, (M, N, K) in enumerate(_random_shapes(4242 + DTYPES.index(dtype), 16)):
+        A, B = si.gen_operands(dtype, M, N, K, seed=5000 + i)
+        rng = np.random.default_rng(i)
+        rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 4)]))
+        ref = oracle_gemm(dtype, A, B, rows=rows)
+        v = mp.select_variant(dtype, M, N, K)
+        vw = mp.select_variant(dtype, M, N, K, with_ws=True)
+        _log(f"random {dtype} {M}x{N}x{K}: {mp.variant_name(dtype, v)} / ws {mp.variant_name(dtype, vw)}")
+        assert_parity(dtype, gpu_gemm(dtype, A, B)[rows], *ref, f"{dtype} {M}x{N}x{K} {mp.variant_name(dtype, v)}")
+        assert_parity(dtype, gpu_gemm(dtype, A, B, workspace="auto")[rows], *ref,
+                      f"{dtype} {M}x{N}x{K} ws {mp.variant_name(dtype, vw)}")
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_splitk_deterministic_and_concurrent(dtype):
     """Split results do not depend on which workgroup finishes last (five
