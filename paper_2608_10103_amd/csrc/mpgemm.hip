@@ -398,8 +398,22 @@ const Pref kPrefF16[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1
                          {V_PIPE64, 1}};
 const Pref kPrefS8[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                         {V_PIPE64, 1}};
+// INT4 on the 256 x 256 kernels (checked by int4_pref_ok): M and N must be
+// multiples of 256 for the one-wave-per-SIMD FP6 kernel and for the in-GEMM
+// E2M3 one (their edge tiles take the general epilogue), which the latter
+// also needs at most one round of tiles or whole rounds (with K >= 4096) and
+// K >= 2048; otherwise, with a workspace, the 8-wave FP6 kernel, and without
+// one the 128 x 128 INT8-MFMA kernel (the 256 x 256 INT8-MFMA one only for
+// whole tiles in whole rounds, where E2M3 cannot run: at 8192^3 415 against
+// 543 us, on ragged shapes mostly slower than 128 x 128). Interleaved on MI355X at 2688 ..
+// 8192 x 2432 .. 8192 x 2048 .. 8192 (44 shapes): with a workspace, on ragged
+// shapes the 8-wave FP6 kernel beat the one-wave-per-SIMD one at all 11
+// (1.02-1.17x); without, the E2M3 kernel was the slowest candidate at every
+// ragged shape and at partial second rounds (4096 x 6144 x 4096: 142.1
+// against 127.4 us for 128 x 128), ahead only in one round (4096^3: 71.9
+// against 79.2 us) or whole rounds (8192 x 4096 x 4096: 151.1 against 173.3).
 const Pref kPrefS4[] = {{V_I4WIDE, 192}, {V_STAGED256_W2X4, 256}, {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
-const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 512}, {V_I4WIDE, 192}, {V_STAGED256_W2X4, 256},
+const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 144}, {V_I4WIDE, 192}, {V_STAGED256_W2X4, 256},
                           {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
 
 // Streaming kernel for problems with a small side (LLM decoding), against the
@@ -522,6 +536,16 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
     return cands[best];
 }
 
+// The conditions of the INT4 256 x 256 preferences (see kPrefS4).
+bool int4_pref_ok(int variant, int M, int N, int K) {
+    const bool whole = M % 256 == 0 && N % 256 == 0;
+    const long tiles = (long)(M / 256) * (N / 256);
+    if (variant == V_FP6_WIDE) return whole;
+    if (variant == V_I4WIDE) return whole && K >= 2048 && (tiles <= 256 || (tiles % 256 == 0 && K >= 4096));
+    if (variant == V_STAGED256_W2X4) return whole && tiles % 256 == 0;
+    return true;
+}
+
 // with_ws: the choice for a call that has a workspace (INT4 may then take
 // the FP6 kernels fed by the conversion pre-pass).
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C,
@@ -563,6 +587,7 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
     for (int i = 0; i < n; ++i) {
         const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
+        if (dtype == S4 && !int4_pref_ok(prefs[i].variant, M, N, K)) continue;
         const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
         // skip a tile that would mostly compute padding
         if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < n) continue;

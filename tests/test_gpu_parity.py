@@ -620,7 +620,9 @@ def test_automatic_choice_random_shapes(dtype):
     """Whatever kernel the entry point picks, with and without a workspace,
     on seeded shapes across every region of the choice: sampled rows against
     the oracle (first, last and four seeded rows)."""
-    for i, (M, N, K) in enumerate(_random_shapes(4242 + DTYPES.index(dtype), 16)):
+    # plus a ragged INT4 shape past 144 tiles of 256 x 256 (the 8-wave FP6
+    # kernel with a workspace, the 128 x 128 one without)
+    for i, (M, N, K) in enumerate(_random_shapes(4242 + DTYPES.index(dtype), 16) + [(3200, 6528, 1024)]):
         A, B = si.gen_operands(dtype, M, N, K, seed=5000 + i)
         rng = np.random.default_rng(i)
         rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 4)]))
