@@ -412,6 +412,14 @@ const Pref kPrefS8[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}
 // ragged shape and at partial second rounds (4096 x 6144 x 4096: 142.1
 // against 127.4 us for 128 x 128), ahead only in one round (4096^3: 71.9
 // against 79.2 us) or whole rounds (8192 x 4096 x 4096: 151.1 against 173.3).
+// The FP6 kernels' gain over 128 x 128 grows with K (whole tiles in one round:
+// 1.12x at K = 2048, 1.37x at 4096, 1.58x at 8192), so the partial last round
+// they can afford does too: the one-wave-per-SIMD kernel needs K >= 3072 or
+// 60% of the CU slots filled (4352 x 4096 x 2048, 272 tiles: 55.8 against
+// 50.7 us), the 8-wave one on ragged shapes 75% from K = 3072, 60% from
+// K = 8192 or three rounds (6784 x 2432 x 4096, 270 tiles: 94.3 against
+// 77.2; 4300 x 4100 x 4096: 100.7 against 92.9; 7040 x 7168 x 2048, 784
+// tiles: 124.5 against 132.6).
 const Pref kPrefS4[] = {{V_I4WIDE, 192}, {V_STAGED256_W2X4, 256}, {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
 const Pref kPrefS4Ws[] = {{V_FP6_WIDE, 144}, {V_FP6_256_S2, 144}, {V_I4WIDE, 192}, {V_STAGED256_W2X4, 256},
                           {V_SPREAD128W8_K64, 1}, {V_PIPE64, 1}};
@@ -539,8 +547,11 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
 // The conditions of the INT4 256 x 256 preferences (see kPrefS4).
 bool int4_pref_ok(int variant, int M, int N, int K) {
     const bool whole = M % 256 == 0 && N % 256 == 0;
-    const long tiles = (long)(M / 256) * (N / 256);
-    if (variant == V_FP6_WIDE) return whole;
+    const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
+    // share of the CU slots the rounds of 256 x 256 tiles keep busy
+    const double fill = (double)tiles / (double)(((tiles + 255) / 256) * 256);
+    if (variant == V_FP6_WIDE) return whole && (K >= 3072 || fill >= 0.6);
+    if (variant == V_FP6_256_S2) return tiles >= 768 || (K >= 3072 && fill >= 0.75) || (K >= 8192 && fill >= 0.6);
     if (variant == V_I4WIDE) return whole && K >= 2048 && (tiles <= 256 || (tiles % 256 == 0 && K >= 4096));
     if (variant == V_STAGED256_W2X4) return whole && tiles % 256 == 0;
     return true;

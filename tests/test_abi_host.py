@@ -268,13 +268,22 @@ def test_skinny_selection():
 
 def test_int4_large_tile_conditions():
     """INT4 on the 256 x 256 kernels: the one-wave-per-SIMD FP6 kernel only
-    for M and N multiples of 256 (else, with a workspace, the 8-wave FP6 one);
-    without a workspace the in-GEMM E2M3 kernel only for whole tiles in one
-    round or in whole rounds (K >= 4096), else the 128 x 128 INT8-MFMA kernel
-    (the 256 x 256 INT8-MFMA one for whole rounds E2M3 cannot run)."""
+    for M and N multiples of 256 (else, with a workspace, the 8-wave FP6 one),
+    each only where its partial last round costs less than the FP6 rate gains
+    at that K; without a workspace the in-GEMM E2M3 kernel only for whole
+    tiles in one round or in whole rounds (K >= 4096), else the 128 x 128
+    INT8-MFMA kernel (the 256 x 256 INT8-MFMA one for whole rounds E2M3
+    cannot run)."""
     name = lambda M, N, K, ws: mp.variant_name("s4", mp.select_variant("s4", M, N, K, with_ws=ws))
-    assert name(3200, 6528, 4096, True) == "fp6pipe256x256_w2x4_k128_s2"      # ragged
+    assert name(2944, 4608, 3328, True) == "fp6pipe256x256_w2x4_k128_s2"      # ragged, 84% filled
+    assert name(7040, 7168, 2048, True) == "fp6pipe256x256_w2x4_k128_s2"      # ragged, 784 tiles
+    assert name(3200, 6528, 8192, True) == "fp6pipe256x256_w2x4_k128_s2"      # ragged, 66%, long K
+    assert name(3200, 6528, 4096, True) == "spread128x128_w2x4_k64_s4"        # ragged, 66%
+    assert name(6784, 2432, 4096, True) == "spread128x128_w2x4_k64_s4"        # ragged, 53%
+    assert name(6272, 3968, 2048, True) == "spread128x128_w2x4_k64_s4"        # ragged, short K
     assert name(4096, 6144, 4096, True).startswith("fp6wide256x256_w2x2_k128_s3")
+    assert name(4608, 4608, 2048, True).startswith("fp6wide256x256_w2x2_k128_s3")  # 63%
+    assert name(4352, 4096, 2048, True).startswith("spread128x128_w2x4_k64_s4")    # 53%, short K
     assert name(6784, 2432, 4096, False) == "spread128x128_w2x4_k64_s4"       # ragged
     assert name(4096, 6144, 4096, False) == "spread128x128_w2x4_k64_s4"       # 1.5 rounds
     assert name(3584, 3584, 3584, False) == "e2m3wide256x256_w2x2_k256"       # one round (196 tiles)
