@@ -384,8 +384,19 @@ struct Pref { int variant; long min_tiles; };
 // shapes.
 // FP16, INT8: the one-wave-per-SIMD kernel first where whole 256 x 256 tiles
 // fill the CUs (1.09-1.21x the 8-wave kernel for FP16, 1.12-1.23x for INT8,
-// at 2048..16384 x 4096..16384 x 2048..16384); the 8-wave kernel, with
-// predicated edges, where M or N is not a multiple of 256. The whole-tile
+// at 2048..16384 x 4096..16384 x 2048..16384). Where M or N is not a
+// multiple of 256 (checked by ragged_pref_ok) both 256 x 256 kernels need the
+// rounds of tiles at least 65% filled, and the one-wave-per-SIMD one also
+// K >= 4096; the 8-wave one is then taken from 144 tiles. Interleaved on
+// MI355X at 38 ragged shapes (1800 .. 12000 x 2432 .. 7168 x 2048 .. 8192):
+// at fill 0.53-0.63 the 128 x 128 kernel was fastest (FP16 6784 x 2432 x
+// 4096: 161.9 against 226.4 us one-wave-per-SIMD, 216.3 8-wave; 4700 x 4300
+// x 6144: 307.7 against 388.4 and 380.2), from 0.66 on the 256 x 256 ones
+// (3700 x 5900 x 4096: 277.0 and 270.1 against 290.0); with
+// K < 4096 the 8-wave kernel beat the one-wave-per-SIMD one at every shape
+// (FP16 7040 x 7168 x 2048: 264.4 against 311.1; 1800 x 7000 x 2048: 69.6
+// against 76.4; INT8 12000 x 3000 x 2048: 122.6 against 136.0); from K =
+// 4096 they were within 7% of each other either way. The whole-tile
 // kernels (this one, and for INT4 the FP6 pre-pass one) are taken from 144
 // tiles (56% of the CUs) up, the INT4 in-GEMM-conversion one from 192: at
 // 2304^3 .. 3840^3 and {4096 x 2048, 2048 x 4096, 4096 x 2560} on MI355X
@@ -394,9 +405,9 @@ struct Pref { int variant; long min_tiles; };
 // 3840^3: 155.8 against 112.2 us); INT4 in-GEMM conversion against the
 // 64-byte eight-wave kernel: 53.0 against 58.9 us at 169 tiles, 61.9
 // against 68.9 at 196.
-const Pref kPrefF16[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
+const Pref kPrefF16[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 144}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                          {V_PIPE64, 1}};
-const Pref kPrefS8[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 256}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
+const Pref kPrefS8[] = {{V_WIDE, 144}, {V_PIPE256_W2X4, 144}, {V_SPREAD128W8, 1}, {V_SPREAD128W8_K64, 1},
                         {V_PIPE64, 1}};
 // INT4 on the 256 x 256 kernels (checked by int4_pref_ok): M and N must be
 // multiples of 256 for the one-wave-per-SIMD FP6 kernel and for the in-GEMM
@@ -557,6 +568,16 @@ bool int4_pref_ok(int variant, int M, int N, int K) {
     return true;
 }
 
+// The conditions of the FP16 and INT8 256 x 256 preferences where M or N is
+// not a multiple of 256 (see kPrefF16).
+bool ragged_pref_ok(int variant, int M, int N, int K) {
+    if ((M % 256 == 0 && N % 256 == 0) || (variant != V_WIDE && variant != V_PIPE256_W2X4)) return true;
+    const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
+    const double fill = (double)tiles / (double)(((tiles + 255) / 256) * 256);
+    if (fill < 0.65) return false;
+    return variant != V_WIDE || K >= 4096;
+}
+
 // with_ws: the choice for a call that has a workspace (INT4 may then take
 // the FP6 kernels fed by the conversion pre-pass).
 int select_variant(int dtype, int M, int N, int K, const void *A, const void *B, const void *C,
@@ -599,6 +620,14 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         const Variant &v = t[prefs[i].variant];
         if (!supports(dtype, v, M, N, K, A, B, C)) continue;
         if (dtype == S4 && !int4_pref_ok(prefs[i].variant, M, N, K)) continue;
+        // (with a workspace, where the stream-K schedule splits the partial
+        // last round, the fill of the rounds does not apply)
+        if (dtype != S4 && !ragged_pref_ok(prefs[i].variant, M, N, K)) {
+            const int tw = sk_twin(prefs[i].variant);
+            if (!(with_ws && tw >= 0 && supports(dtype, t[tw], M, N, K, A, B, C) && sk_plan(dtype, t[tw], M, N, K).on &&
+                  (prefs[i].variant != V_WIDE || K >= 4096)))
+                continue;
+        }
         const long tm = (M + v.bm - 1) / v.bm, tn = (N + v.bn - 1) / v.bn;
         // skip a tile that would mostly compute padding
         if (4 * (long)M * N < 3 * tm * v.bm * tn * v.bn && i + 1 < n) continue;

@@ -156,9 +156,17 @@ def test_selection_at_sweep_sizes():
     for n in (512, 1024, 2048):
         assert mp.select_variant("s4", n, n, n, with_ws=True) == mp.select_variant("s4", n, n, n)
     # ragged edges: the one-wave-per-SIMD kernel (its panels bounded by the
-    # rows inside the matrix); K off its 128-byte slices: the 64-byte kernels
-    assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "wide256x256_w2x2_k128_m16"
-    assert mp.variant_name("s8", mp.select_variant("s8", 4000, 4400, 6400)) == "wide256x256_w2x2_k128_m16"
+    # rows inside the matrix) where the rounds of 256 x 256 tiles are at least
+    # 60% filled and K >= 4096, the 8-wave one for shorter K, the 128 x 128
+    # kernel below 60%; K off its 128-byte slices: the 64-byte kernels
+    assert mp.variant_name("f16", mp.select_variant("f16", 7000, 7000, 7168)) == "wide256x256_w2x2_k128_m16"
+    assert mp.variant_name("f16", mp.select_variant("f16", 1800, 7000, 2048)) == "pipe256x256_w2x4_k128_s2"
+    assert mp.variant_name("s8", mp.select_variant("s8", 7040, 7168, 2048)) == "pipe256x256_w2x4_k128_s2"
+    assert mp.variant_name("f16", mp.select_variant("f16", 4096 + 64, 4096, 4096)) == "spread128x128_w2x4_k128_s4"
+    assert mp.variant_name("s8", mp.select_variant("s8", 6784, 2432, 4096)) == "spread128x128_w2x4_k128_s4"
+    assert mp.variant_name("s8", mp.select_variant("s8", 4000, 4400, 6400)) == "spread128x128_w2x4_k128_s4"
+    # with a workspace the stream-K schedule splits the partial last round
+    assert mp.variant_name("s8", mp.select_variant("s8", 4000, 4400, 6400, with_ws=True)).startswith("wide256x256")
     assert mp.variant_name("s8", mp.select_variant("s8", 8000, 8000, 8000)) == "spread128x128_w2x4_k64_s4"
 
 

@@ -172,7 +172,9 @@ def test_sk_selection_with_a_workspace():
     for d, M, N, K, plain, twin in [
         ("f16", 4352, 4096, 8192, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
         ("s8", 4352, 4096, 16384, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
-        ("f16", 4000, 4400, 6400, "wide256x256_w2x2_k128_m16", "wide256x256_w2x2_k128_m16_sk"),
+        # ragged, 288 tiles (rounds 56% filled): without a workspace the
+        # 128 x 128 kernel, with one the stream-K schedule of the 256 x 256 one
+        ("f16", 4000, 4400, 6400, "spread128x128_w2x4_k128_s4", "wide256x256_w2x2_k128_m16_sk"),
         ("s8", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
         ("s4", 2100, 2000, 12800, "spread128x128_w2x4_k64_s4", "spread128x128_w2x4_k64_s4_sk"),
         ("f16", 2100, 2000, 6400, "spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4_sk"),
