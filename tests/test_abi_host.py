@@ -338,12 +338,17 @@ def test_narrow_selection():
         # kernel taken before, FP16 / INT8 / INT4)
         (512, 4096, 4096): ("spread64x128_w2x4_k128_s4",) * 3,
         (4096, 512, 4096): ("spread128x64_w4x2_k128_s4",) * 3,
-        (384, 2048, 4096): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
-        (512, 2048, 8192): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,  # unsplit
+        # above 256 rows, 64 x 64 tiles in one round (at most 256) and at
+        # least 32 slices: the eight-slice ring (FP16 and INT8; 1.03-1.34x
+        # the four-slice candidates at 30 of 50 measured shapes)
+        (384, 2048, 4096): ("spread64x64_w2x2_k128_s8_m16",) * 2 + ("spread64x64_w2x2_k128_s4_m16",),
+        (512, 2048, 8192): ("spread64x64_w2x2_k128_s8_m16",) * 2 + ("spread64x64_w2x2_k128_s4_m16",),  # unsplit
+        (384, 2048, 2048): ("spread64x64_w2x2_k128_s8_m16",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,  # INT8: 16 slices
         # from 257 rows, wherever 128 x 128 tiles would fill under half the CUs
         # (FP16 above 256 rows: the eight-wave 64 x 128 rather than 64 x 64)
-        (1024, 1024, 4096): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
-        (768, 768, 8192): ("spread64x128_w2x4_k128_s4",) + ("spread64x64_w2x2_k128_s4_m16",) * 2,
+        (1024, 1024, 4096): ("spread64x64_w2x2_k128_s8_m16",) * 2 + ("spread64x64_w2x2_k128_s4_m16",),
+        (768, 768, 8192): ("spread64x64_w2x2_k128_s8_m16",) * 2 + ("spread64x64_w2x2_k128_s4_m16",),
+        (1100, 1300, 4096): ("spread64x128_w2x4_k128_s4",) * 3,          # 378 tiles of 64 x 64
         (1280, 1280, 4096): ("spread64x128_w2x4_k128_s4",) * 3,          # 100 tiles of 128 x 128
         (1408, 1408, 2048): ("spread64x128_w2x4_k128_s4",) * 3,          # 121
         (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
