@@ -629,6 +629,12 @@ int select_variant(int dtype, int M, int N, int K, const void *A, const void *B,
         if (dtype == S4 && !int4_pref_ok(prefs[i].variant, M, N, K)) continue;
         // (with a workspace, where the stream-K schedule splits the partial
         // last round, the fill of the rounds does not apply)
+        // INT8 with K <= 2048 (at most 16 slices of 128 bytes) past one round
+        // of 128 x 128 tiles: the 64-byte-slice kernel (twice the slices to
+        // pipeline). Interleaved on MI355X at 14 shapes: 1.02-1.22x faster
+        // with 384 .. 512 tiles (2304 x 3456 x 2048: 29.3 against 35.7 us),
+        // 0.965-0.996x with 144 .. 256 tiles or K = 3072, 4096.
+        if (dtype == S8 && prefs[i].variant == V_SPREAD128W8 && K <= 2048 && tile_count(v, M, N) > 256) continue;
         if (dtype != S4 && !ragged_pref_ok(prefs[i].variant, M, N, K)) {
             const int tw = sk_twin(prefs[i].variant);
             if (!(with_ws && tw >= 0 && supports(dtype, t[tw], M, N, K, A, B, C) && sk_plan(dtype, t[tw], M, N, K).on &&

@@ -562,3 +562,15 @@ def test_workspace_arguments_rejected_on_host():
     v = mp.select_variant("s8", 64, 1000, 8192)
     assert L.mpgemm_run_variant_ws(1, v, 2, 64, 1000, 8192, A, B, C, None, None, 0, None) == 1
     assert L.mpgemm_run_variant_ws(1, v, -1, 64, 1000, 8192, A, B, C, None, None, 0, None) == 1
+
+
+def test_int8_short_k_takes_64_byte_slices_past_one_round():
+    """INT8 with K <= 2048 and more than 256 tiles of 128 x 128: the
+    64-byte-slice kernel (measured 1.02-1.22x faster there on MI355X); one
+    round or longer K: the 128-byte one."""
+    name = lambda M, N, K: mp.variant_name("s8", mp.select_variant("s8", M, N, K))
+    assert name(2048, 4096, 2048) == "spread128x128_w2x4_k64_s4"
+    assert name(2304, 3456, 2048) == "spread128x128_w2x4_k64_s4"
+    assert name(2048, 2048, 2048) == "spread128x128_w2x4_k128_s4"   # 256 tiles
+    assert name(2560, 2560, 4096) == "spread128x128_w2x4_k128_s4"   # 32 slices
+    assert mp.variant_name("f16", mp.select_variant("f16", 2048, 4096, 2048)) == "spread128x128_w2x4_k128_s4"
