@@ -536,16 +536,17 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
     // ones), with at least 64 slices of K and 128 to 256 workgroups, and with
     // more than 192 only from 128 slices on (224 tiles at 14336 x 4096: 4-6%
     // slower); INT4, with its nibble unpacking, gained at no measured shape.
-    // Above 256 rows (never split) they gain wherever their tiles fit one
-    // round, from 32 slices: 64 x 64 at 900 x 900 x 8192 32.1 against 40.1
-    // us for 64 x 128 (FP16), 18.6 against 20.3 for four-slice 64 x 64
-    // (INT8); 1024 x 1024 x 8192 32.9 against 41.0 (FP16); 32 x 64 at 700 x
-    // 700 x 8192 26.8 against 36.2; 900 x 900 x 4096 INT8 11.6 against 12.2.
-    // With more tiles (1100 x 1300, 384 .. 1200 x 1200 .. 4096) they lose.
+    // Above 128 rows they gain wherever their tiles fit one round, from 32
+    // slices: 64 x 64 at 900 x 900 x 8192 32.1 against 40.1 us for 64 x 128
+    // (FP16), 18.6 against 20.3 for four-slice 64 x 64 (INT8); 1024 x 1024 x
+    // 8192 32.9 against 41.0 (FP16); 32 x 64 at 700 x 700 x 8192 26.8
+    // against 36.2; 160 x 4096 x 8192 29.5 against 38.5 for 128 x 128 split
+    // in two (FP16); 192 x 2048 x 4096 INT8 9.9 against 13.9. With more
+    // tiles (1100 x 1300, 384 .. 1200 x 1200 .. 4096) they lose.
     int deep = -1;
     double deep_cost = 0;
     const long slices = kb / 128;
-    const bool wide_small = small > 256;
+    const bool wide_small = small > 128;
     if (dtype != S4 && ((small <= 128 && slices >= 64) || (wide_small && slices >= 32))) {
         const int dmir = M <= N ? 0 : 2;
         for (int cand : {V_DEEP + dmir, V_DEEP + 1 + dmir, V_DEEP + 4}) {
@@ -554,7 +555,10 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
             if (tiles < 128 || tiles > 256 || (!wide_small && tiles > 192 && slices < 128) ||
                 !supports(dtype, v, M, N, K, A, B, C))
                 continue;
-            const double c = 0.7 * (v.bm + v.bn) * kb;
+            // above 128 rows the four-slice candidates' split-K costs its
+            // fix-up too: scaled by 0.5 (192 x 2048 x 4096: 15.0 against
+            // 19.2 us for 128 x 128 split in four, whose cost is lower at 0.7)
+            const double c = (wide_small ? 0.5 : 0.7) * (v.bm + v.bn) * kb;
             if (deep < 0 || c < deep_cost) deep = cand, deep_cost = c;
         }
     }

@@ -352,7 +352,10 @@ def test_narrow_selection():
         (1280, 1280, 4096): ("spread64x128_w2x4_k128_s4",) * 3,          # 100 tiles of 128 x 128
         (1408, 1408, 2048): ("spread64x128_w2x4_k128_s4",) * 3,          # 121
         (384, 14336, 4096): ("spread128x128_w2x4_k128_s4",) * 2 + ("spread128x128_w2x4_k64_s4",),
-        (256, 4096, 14336): ("spread128x128_w2x4_k128_s4", "spread128x128_w2x4_k128_s4", "spread64x64_w2x2_k128_s4_m16"),
+        # 129 .. 256 rows, 64 x 64 tiles in one round: the eight-slice ring
+        # (FP16 256 x 4096 x 4096: 18.6 against 22.7 us)
+        (256, 4096, 14336): ("spread64x64_w2x2_k128_s8_m16",) * 2 + ("spread64x64_w2x2_k128_s4_m16",),
+        (192, 2048, 4096): ("spread32x64_w1x2_k128_s8_m16",) * 2 + ("spread128x128_w2x4_k64_s4",),
     }
     for (M, N, K), names in want.items():
         assert tuple(name(dt, M, N, K) for dt in ("f16", "s8", "s4")) == names, (M, N, K)
@@ -395,7 +398,8 @@ def test_split_k_selection():
     assert split("f16", "spread128x128_w2x4_k128_s4", 128, 8192, 8192) == 2   # the narrow tiles' rule
     assert split("s8", "spread32x128_w1x4_k128_s4_m16", 32, 8192, 8192) == 2
     assert sel("f16", 32, 8192, 8192) == 1     # the eight-slice ring instead
-    assert sel("f16", 256, 4096, 14336) == 2
+    assert split("f16", "spread128x128_w2x4_k128_s4", 256, 4096, 14336) == 2
+    assert sel("f16", 256, 4096, 14336) == 1   # the eight-slice 64 x 64 tiles instead
     assert sel("f16", 64, 4096, 8192) == 4     # 32 tiles
     assert sel("s8", 32, 14336, 4096) == 1     # 224 tiles of 32 x 64
     assert sel("s8", 128, 8192, 8192) == 1
