@@ -531,11 +531,12 @@ int select_narrow(int dtype, int M, int N, int K, const void *A, const void *B, 
     // LDS) in a single round: the same tile streams its rows 1.1-1.3x faster
     // than through the four-slice ring at 16 ... 128 x 8192 x 8192 (FP16,
     // INT8), so its cost is scaled by 0.7 against the four-slice candidates,
-    // split or not. Measured on MI355X, it gains only up to 128 rows on the
-    // small side (at 256 its tiles copy twice the bytes of the 128 x 128
-    // ones), with at least 64 slices of K and 128 to 256 workgroups, and with
+    // split or not. Measured on MI355X, up to 128 rows on the small side it
+    // gains with at least 64 slices of K and 128 to 256 workgroups, and with
     // more than 192 only from 128 slices on (224 tiles at 14336 x 4096: 4-6%
-    // slower); INT4, with its nibble unpacking, gained at no measured shape.
+    // slower); never where its tiles need more than one round (256 x 8192:
+    // they copy twice the bytes of 128 x 128 ones); INT4, with its nibble
+    // unpacking, gained at no measured shape.
     // Above 128 rows they gain wherever their tiles fit one round, from 32
     // slices: 64 x 64 at 900 x 900 x 8192 32.1 against 40.1 us for 64 x 128
     // (FP16), 18.6 against 20.3 for four-slice 64 x 64 (INT8); 1024 x 1024 x
