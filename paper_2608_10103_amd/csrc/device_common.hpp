@@ -278,10 +278,12 @@ __global__ __launch_bounds__(256) void row_sums(const uint8_t *__restrict__ X, i
 
 // Rank of workgroup `id` of `n` in an order where each XCD owns a
 // contiguous run: workgroups are dispatched round-robin over the 8 XCDs,
-// each with its own L2, so ids id, id + 8, ... share one. The identity when
-// n is not a multiple of 8.
+// each with its own L2, so ids id, id + 8, ... share one. XCD x runs
+// n / 8 workgroups, one more when x < n % 8; its run starts after the runs
+// of XCDs 0 .. x - 1 (a bijection on 0 .. n - 1).
 __device__ __forceinline__ int xcd_rank(int id, int n) {
-    return (n & 7) ? id : (id & 7) * (n >> 3) + (id >> 3);
+    const int x = id & 7, j = id >> 3, q = n >> 3, r = n & 7;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
 }
 
 // Linear tile index -> (tile row, tile column), walking group_m tile rows
